@@ -1,0 +1,242 @@
+/*
+ * easybalance.h -- C ABI of libeasybalance.so, the one-GPU hot path of
+ * EasyBalance (cross-layer load balancing for expert-parallel MoE inference,
+ * arXiv 2608.07964) on AMD Instinct MI355X (gfx950).
+ *
+ * Algorithm 1 of the paper runs, per step, three operations:
+ *   Attn_Route_Dispatch(RunSet_{i-1})  -> easybalance_route (routing part)
+ *   RunSet_i = Schedule(S_{i-1}, m)    -> easybalance_schedule
+ *   MoECompute_Combine(RunSet_i)       -> easybalance_moe_step + easybalance_combine
+ * The expert-parallel group of D devices is virtual: all experts of all layers
+ * live on this one GPU, E/D contiguous experts per virtual device, and the work
+ * every virtual device would do in a step runs in one grouped launch.
+ *
+ * Conventions shared by every call
+ *  - Return value: EB_OK (0) or a negative EB_ERR_* code.  On error the
+ *    outputs are unspecified and easybalance_last_error() (thread-local)
+ *    describes the first failed check.  No C++ exception crosses the ABI.
+ *  - Memory: every buffer is owned by the caller.  "device" pointers are HIP
+ *    device allocations on the current device; "host" pointers are ordinary
+ *    host memory.  The library allocates no device memory; scratch space of
+ *    easybalance_moe_step is a caller workspace sized by
+ *    easybalance_moe_step_workspace_size.
+ *  - Streams: `stream` is a hipStream_t passed as void* (NULL = null stream).
+ *    Device calls only enqueue work on it and never synchronize; the caller
+ *    orders calls on one stream or with events.
+ *  - Layouts are row-major and densely packed.  "dtype" is the model's storage
+ *    type (EB_DTYPE_F32 or EB_DTYPE_BF16, bf16 as raw 16-bit patterns);
+ *    accumulation is always fp32.
+ *  - Shape limits (EB_ERR_UNSUPPORTED otherwise): H % 256 == 0,
+ *    F % 128 == 0, 1 <= k <= E, E + S <= 1024, E % D == 0, L <= EB_MAX_LAYERS,
+ *    L * (E + S) <= 15360.
+ */
+#ifndef EASYBALANCE_H
+#define EASYBALANCE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define EB_OK 0
+#define EB_ERR_INVALID_ARG (-1)
+#define EB_ERR_UNSUPPORTED (-2)
+#define EB_ERR_HIP (-3)
+#define EB_ERR_WORKSPACE_TOO_SMALL (-4)
+
+#define EB_DTYPE_F32 0
+#define EB_DTYPE_BF16 1
+
+#define EB_POLICY_MAXUTIL 0
+#define EB_POLICY_CUMUTIL 1
+#define EB_POLICY_DIFFPEAK 2
+
+#define EB_MAX_POOL 64          /* micro-batch ids are 0..63 (one bit each)   */
+#define EB_MAXUTIL_MAX_POOL 20  /* MaxUtil enumerates 2^n subsets             */
+#define EB_MAX_RUN 64
+#define EB_MAX_LAYERS 128
+
+/* Kernel classes reported by the profiling calls. */
+#define EB_K_ROUTE_NORM 0
+#define EB_K_ROUTE_LOGITS 1
+#define EB_K_ROUTE_TOPK 2
+#define EB_K_PERM_COUNT 3
+#define EB_K_PERM_SCAN 4
+#define EB_K_PERM_SCATTER 5
+#define EB_K_GATEUP 6
+#define EB_K_DOWN 7
+#define EB_K_COMBINE 8
+#define EB_NUM_KERNELS 9
+
+/* Model shape.  L MoE layers, hidden H, expert FFN size F, E routed experts
+ * with top-k routing, S always-on shared experts, D virtual EP devices.
+ * rms_eps: RMSNorm epsilon.  norm_topk: 0 = routing weights are the softmax
+ * over all E experts taken at the k picks (Eq. 1 as written), 1 = renormalised
+ * over the k picks. */
+typedef struct eb_model_desc {
+  int32_t L, H, F, E, k, S, D;
+  int32_t dtype;
+  float rms_eps;
+  int32_t norm_topk;
+} eb_model_desc;
+
+/* One micro-batch of a step's RunSet, at its own layer (Algorithm 1 keeps
+ * l_j per micro-batch; Section 4.1 lets micro-batches at different layers run
+ * jointly).  All pointers are device pointers produced by easybalance_route
+ * for this micro-batch at `layer`. */
+typedef struct eb_work {
+  int32_t mb_id;        /* micro-batch id j (informational)              */
+  int32_t layer;        /* l_j, 0 <= layer < L                           */
+  int32_t T;            /* tokens, >= 0                                  */
+  int32_t reserved;     /* must be 0                                     */
+  const void* a;        /* [T][H] dtype: normalised activations          */
+  const int32_t* idx;   /* [T][k] routed expert ids                      */
+  const float* w;       /* [T][k] routing weights                        */
+} eb_work;
+
+/* Optional extra outputs of easybalance_moe_step (any member may be NULL;
+ * a NULL member lives in the workspace instead).  P = sum_rho T_rho * (k+S). */
+typedef struct eb_step_views {
+  void* a_perm;         /* [P][H] dtype: rows grouped by (layer, expert)  */
+  void* h;              /* [P][F] dtype: SwiGLU activations               */
+  int32_t* perm;        /* [P]: pair index at each grouped position       */
+  int32_t* offsets;     /* [L*(E+S)+1]: first grouped row of each key     */
+} eb_step_views;
+
+/* Library version string, e.g. "easybalance-mi355x 0.1.0". */
+const char* easybalance_version(void);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* easybalance_last_error(void);
+
+/*
+ * easybalance_route -- RMSNorm, router and top-k of one micro-batch at one
+ * layer: the routing half of Attn_Route_Dispatch (Algorithm 1), i.e.
+ * W_l, I_l = topk(G(h'_l)) of Section 2.1, plus the expert pair counts from
+ * which the per-device workload vector of Section 2.3 is formed.
+ *
+ *   a   = dtype( x * r * gain ),  r = 1 / sqrt(mean(x^2) + rms_eps)   per token
+ *   z   = a Wg^T + bias                                  (fp32 accumulate)
+ *   idx = the k largest z per token, largest first; equal z -> lower expert id
+ *   w   = softmax(z over all E)[idx]   (norm_topk=1: renormalised over the k)
+ *   counts[e] = #{(t, r) : idx[t][r] == e}
+ *
+ * layer      0 <= layer < L (checked; weights are passed for this layer)
+ * T          tokens (>= 0)
+ * x          device [T][H] fp32 residual stream (read only)
+ * gain       device [H] fp32 RMSNorm gain
+ * Wg         device [E][H] dtype router weights
+ * bias       device [E] fp32 router logit bias
+ * a_out      device [T][H] dtype
+ * logits_out device [T][E] fp32 (required: the router's output z)
+ * idx_out    device [T][k] int32
+ * w_out      device [T][k] fp32
+ * counts_out device [E] int32 (overwritten, not accumulated)
+ * Non-finite logits give unspecified (but in-range) picks.
+ */
+int easybalance_route(const eb_model_desc* desc, int32_t layer, int32_t T, const float* x,
+                      const float* gain, const void* Wg, const float* bias, void* a_out,
+                      float* logits_out, int32_t* idx_out, float* w_out, int32_t* counts_out,
+                      void* stream);
+
+/*
+ * easybalance_schedule -- RunSet_i = Schedule(S_{i-1}, m) of Algorithm 1.
+ * Host only, pure, re-entrant; no GPU access.
+ *
+ * Workload of micro-batch pool_ids[i] (Section 2.3): for device d,
+ *   load_i[d] = sum over experts e in [d*E/D, (d+1)*E/D) of counts[i*E + e].
+ * Utilization of a set R (Eq. 3 for one step): U(R) = sum_d W_d / (D max_d W_d)
+ * with W = sum_{i in R} load_i; U = 1 if W is all zero.
+ *   EB_POLICY_MAXUTIL (Section 4.2): the R with |R| >= min(m, n_pool) of
+ *     highest U; ties -> larger |R| -> lexicographically smallest id list.
+ *     n_pool <= EB_MAXUTIL_MAX_POOL.
+ *   EB_POLICY_CUMUTIL (Section 5.2): scan ids ascending, take the first, add
+ *     each next one iff it strictly raises U.
+ *   EB_POLICY_DIFFPEAK (Section 5.2): scan ids ascending, take the first, add
+ *     each next one iff its peak device (lowest index among maxima) is not yet
+ *     a peak of the chosen set.
+ *   CumUtil/DiffPeak then pad with the lowest unchosen ids up to min(m, n_pool).
+ * All comparisons are exact integer arithmetic.
+ *
+ * n_pool      0 <= n_pool <= EB_MAX_POOL (0 gives an empty RunSet)
+ * pool_ids    host [n_pool], strictly ascending, each in [0, 64)
+ * counts      host [n_pool][E] int32 >= 0, row i belongs to pool_ids[i]
+ * m           >= 1
+ * runset_mask host out: bit j set iff micro-batch j runs in this step
+ * step_load   host out [D] int64 (nullable): combined workload W of the RunSet
+ */
+int easybalance_schedule(int32_t n_pool, const int32_t* pool_ids, const int32_t* counts,
+                         int32_t E, int32_t D, int32_t m, int32_t policy,
+                         uint64_t* runset_mask, int64_t* step_load);
+
+/* Workspace bytes easybalance_moe_step needs for these per-entry token
+ * counts (host [n_run]), assuming every eb_step_views member is NULL. */
+int easybalance_moe_step_workspace_size(const eb_model_desc* desc, int32_t n_run,
+                                        const int32_t* T, size_t* bytes);
+
+/*
+ * easybalance_moe_step -- the expert half of MoECompute_Combine(RunSet_i)
+ * (Algorithm 1): every (token, expert) pair of every micro-batch in the step,
+ * whatever its layer, through its expert in one grouped launch per GEMM
+ * (Section 4.1, cross-layer workload combination).  On a real EP group this
+ * is dispatch all-to-all -> expert FFNs -> gather all-to-all (Section 2.2);
+ * here the dispatch is a stable grouping of the pairs by key
+ * (layer, expert slot), slot E+s being shared expert s:
+ *   pairs enumerated entry by entry in `run` order, then token, then slot
+ *   (k routed slots, then S shared), q = global pair index;
+ *   key(q) = layer * (E+S) + slot expert;  grouped position inv[q] = stable
+ *   rank of q by key;  a_perm[inv[q]] = a of q's token.
+ * For each group g = (l, e):   (W_gu rows 0..F-1 gate, F..2F-1 up)
+ *   h = dtype( SiLU(a_perm W_gate^T) * (a_perm W_up^T) ),  o = dtype( h W_down^T ).
+ * Every row is computed with the same K order whatever group or tile it sits
+ * in, so results do not depend on the schedule (batch invariance).
+ *
+ * run      host [n_run] (1 <= n_run <= EB_MAX_RUN); `run` order defines q
+ * W_gu     host [L] of device pointers, each [E+S][2F][H] dtype
+ * W_dn     host [L] of device pointers, each [E+S][H][F] dtype
+ * ws       device workspace of ws_bytes >= easybalance_moe_step_workspace_size
+ *          (else EB_ERR_WORKSPACE_TOO_SMALL); 256-byte aligned
+ * o_out    device [P][H] dtype: expert outputs at grouped positions
+ * inv_out  device [P] int32: grouped position of pair q
+ * views    host pointer to optional outputs (nullable)
+ * Expert ids outside [0, E) in idx are clamped into range (no fault).
+ */
+int easybalance_moe_step(const eb_model_desc* desc, int32_t n_run, const eb_work* run,
+                         const void* const* W_gu, const void* const* W_dn, void* ws,
+                         size_t ws_bytes, void* o_out, int32_t* inv_out,
+                         const eb_step_views* views, void* stream);
+
+/*
+ * easybalance_combine -- the weighted sum of Eq. (1) plus the residual of
+ * Section 2.1, for every micro-batch of the step (the gather half of
+ * MoECompute_Combine):
+ *   x[t] <- x[t] + ( sum_{r<k} w[t][r] * o[inv[q(t,r)]] + sum_{s<S} o[inv[q(t,k+s)]] )
+ * summed in fp32 in exactly that order (routed slots ascending, then shared).
+ *
+ * run, n_run  the same array passed to easybalance_moe_step
+ * x_inout     host [n_run] of device pointers, entry rho -> [T_rho][H] fp32
+ * o, inv      device outputs of that easybalance_moe_step call
+ */
+int easybalance_combine(const eb_model_desc* desc, int32_t n_run, const eb_work* run,
+                        float* const* x_inout, const void* o, const int32_t* inv,
+                        void* stream);
+
+/*
+ * Kernel timing for measurement.  Between easybalance_profile_begin() and
+ * easybalance_profile_end(), every kernel the library launches is bracketed
+ * by HIP events recorded on the stream it is launched on.  profile_end waits
+ * for those events and returns, per kernel class EB_K_*, the summed duration
+ * in ms (ms_out[EB_NUM_KERNELS]) and the launch count
+ * (launches_out[EB_NUM_KERNELS]); both host arrays are nullable.  Process-wide
+ * state, guarded by a mutex.
+ */
+int easybalance_profile_begin(void);
+int easybalance_profile_end(double* ms_out, int64_t* launches_out);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EASYBALANCE_H */

@@ -1,0 +1,361 @@
+// C ABI of libeasybalance.so: argument checks, workspace layout, per-step
+// tables, kernel-timing hooks.  The compute lives in the kernels of
+// route.hip, permute.hip, gemm.hip and combine.hip; the scheduler in
+// schedule.cpp.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <atomic>
+#include <mutex>
+#include <vector>
+
+#include "eb_internal.h"
+
+namespace eb {
+
+namespace {
+thread_local char g_err[512] = "";
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+int check_desc(const eb_model_desc* d) {
+  if (d == nullptr) return set_error(EB_ERR_INVALID_ARG, "desc is NULL");
+  if (d->L < 1 || d->H < 1 || d->F < 1 || d->E < 1 || d->k < 1 || d->S < 0 || d->D < 1)
+    return set_error(EB_ERR_INVALID_ARG, "desc has a non-positive size (L=%d H=%d F=%d E=%d k=%d S=%d D=%d)",
+                     d->L, d->H, d->F, d->E, d->k, d->S, d->D);
+  if (d->dtype != EB_DTYPE_F32 && d->dtype != EB_DTYPE_BF16)
+    return set_error(EB_ERR_INVALID_ARG, "dtype %d is not EB_DTYPE_F32/BF16", d->dtype);
+  if (d->k > d->E) return set_error(EB_ERR_INVALID_ARG, "k=%d > E=%d", d->k, d->E);
+  if (d->E % d->D != 0) return set_error(EB_ERR_INVALID_ARG, "E=%d not a multiple of D=%d", d->E, d->D);
+  if (!(d->rms_eps >= 0.f)) return set_error(EB_ERR_INVALID_ARG, "rms_eps must be >= 0");
+  if (d->norm_topk != 0 && d->norm_topk != 1) return set_error(EB_ERR_INVALID_ARG, "norm_topk must be 0/1");
+  if (d->H % 256 != 0) return set_error(EB_ERR_UNSUPPORTED, "H=%d is not a multiple of 256", d->H);
+  if (d->F % 128 != 0) return set_error(EB_ERR_UNSUPPORTED, "F=%d is not a multiple of 128", d->F);
+  if (d->E + d->S > 1024) return set_error(EB_ERR_UNSUPPORTED, "E+S=%d > 1024", d->E + d->S);
+  if (d->k + d->S > kMaxSlots) return set_error(EB_ERR_UNSUPPORTED, "k+S=%d > %d", d->k + d->S, kMaxSlots);
+  if (d->L > EB_MAX_LAYERS) return set_error(EB_ERR_UNSUPPORTED, "L=%d > %d", d->L, EB_MAX_LAYERS);
+  if ((long)d->L * (d->E + d->S) > 15360)
+    return set_error(EB_ERR_UNSUPPORTED, "L*(E+S)=%ld > 15360", (long)d->L * (d->E + d->S));
+  return EB_OK;
+}
+
+// Sizes that fix the workspace layout of one step.
+struct StepShape {
+  int n_chunks;
+  long long P;         // grouped rows
+  long long tokens;
+  int max_tiles;
+};
+
+StepShape step_shape(const eb_model_desc& d, int n_run, const int32_t* T) {
+  StepShape s{0, 0, 0, 0};
+  for (int i = 0; i < n_run; ++i) {
+    s.n_chunks += (T[i] + kPermChunk - 1) / kPermChunk;
+    s.tokens += T[i];
+  }
+  s.P = s.tokens * (d.k + d.S);
+  const long long bm = gemm_bm(d.dtype);
+  const long long groups = (long long)n_run * (d.E + d.S);
+  s.max_tiles = (int)((s.P + bm - 1) / bm + (groups < s.P ? groups : s.P));
+  return s;
+}
+
+struct WsLayout {
+  size_t hist, chunk_base, offsets, tiles, n_tiles, perm, a_perm, h, total;
+};
+
+WsLayout ws_layout(const eb_model_desc& d, const StepShape& s, const eb_step_views* v) {
+  const size_t eb = d.dtype == EB_DTYPE_BF16 ? 2 : 4;
+  WsLayout w{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += align_up(bytes);
+    return o;
+  };
+  w.hist = take(sizeof(int32_t) * (size_t)s.n_chunks * d.E);
+  w.chunk_base = take(sizeof(int32_t) * (size_t)s.n_chunks * (d.E + d.S));
+  w.offsets = (v && v->offsets) ? 0 : take(sizeof(int32_t) * ((size_t)d.L * (d.E + d.S) + 1));
+  w.tiles = take(sizeof(int2) * (size_t)(s.max_tiles > 0 ? s.max_tiles : 1));
+  w.n_tiles = take(sizeof(int32_t));
+  w.perm = (v && v->perm) ? 0 : take(sizeof(int32_t) * (size_t)s.P);
+  w.a_perm = (v && v->a_perm) ? 0 : take(eb * (size_t)s.P * d.H);
+  w.h = (v && v->h) ? 0 : take(eb * (size_t)s.P * d.F);
+  w.total = off;
+  return w;
+}
+
+int check_run(const eb_model_desc& d, int32_t n_run, const eb_work* run, bool need_idx) {
+  if (n_run < 1 || n_run > EB_MAX_RUN)
+    return set_error(EB_ERR_INVALID_ARG, "n_run=%d outside [1, %d]", n_run, EB_MAX_RUN);
+  if (run == nullptr) return set_error(EB_ERR_INVALID_ARG, "run is NULL");
+  long long tokens = 0;
+  for (int i = 0; i < n_run; ++i) {
+    const eb_work& r = run[i];
+    if (r.layer < 0 || r.layer >= d.L)
+      return set_error(EB_ERR_INVALID_ARG, "run[%d].layer=%d outside [0, %d)", i, r.layer, d.L);
+    if (r.T < 0) return set_error(EB_ERR_INVALID_ARG, "run[%d].T=%d < 0", i, r.T);
+    if (r.reserved != 0) return set_error(EB_ERR_INVALID_ARG, "run[%d].reserved must be 0", i);
+    if (r.T > 0 && (r.w == nullptr || (need_idx && (r.a == nullptr || r.idx == nullptr))))
+      return set_error(EB_ERR_INVALID_ARG, "run[%d] has a NULL a/idx/w pointer", i);
+    tokens += r.T;
+  }
+  if (tokens * (d.k + d.S) > 0x7fffffffLL)
+    return set_error(EB_ERR_UNSUPPORTED, "step has %lld pairs (> 2^31-1)", tokens * (d.k + d.S));
+  return EB_OK;
+}
+
+RunTable make_run_table(const eb_model_desc& d, int32_t n_run, const eb_work* run,
+                        float* const* x) {
+  RunTable rt;
+  memset(&rt, 0, sizeof(rt));
+  rt.n = n_run;
+  rt.E = d.E;
+  rt.k = d.k;
+  rt.S = d.S;
+  rt.L = d.L;
+  rt.H = d.H;
+  rt.chunk_base[0] = 0;
+  rt.tok_base[0] = 0;
+  for (int i = 0; i < n_run; ++i) {
+    rt.chunk_base[i + 1] = rt.chunk_base[i] + (run[i].T + kPermChunk - 1) / kPermChunk;
+    rt.tok_base[i + 1] = rt.tok_base[i] + run[i].T;
+    rt.layer[i] = run[i].layer;
+    rt.idx[i] = run[i].idx;
+    rt.a[i] = run[i].a;
+    rt.w[i] = run[i].w;
+    rt.x[i] = x ? x[i] : nullptr;
+  }
+  return rt;
+}
+
+int hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return EB_OK;
+  return set_error(EB_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// ---- kernel timing ---------------------------------------------------------
+struct EventPair {
+  hipEvent_t start, stop;
+  int kind;
+};
+std::mutex g_prof_mu;
+std::atomic<bool> g_prof_on{false};
+std::vector<EventPair> g_prof_done;
+std::vector<hipEvent_t> g_prof_free;
+thread_local hipEvent_t t_pending = nullptr;
+
+hipEvent_t prof_event() {
+  if (!g_prof_free.empty()) {
+    hipEvent_t e = g_prof_free.back();
+    g_prof_free.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+}  // namespace
+
+int set_error(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+void prof_start(int kind, hipStream_t s) {
+  (void)kind;
+  if (!g_prof_on.load(std::memory_order_relaxed)) return;
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  t_pending = prof_event();
+  if (t_pending && hipEventRecord(t_pending, s) != hipSuccess) {
+    g_prof_free.push_back(t_pending);
+    t_pending = nullptr;
+  }
+}
+
+void prof_stop(int kind, hipStream_t s) {
+  if (!g_prof_on.load(std::memory_order_relaxed) || t_pending == nullptr) return;
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  hipEvent_t stop = prof_event();
+  if (stop != nullptr && hipEventRecord(stop, s) == hipSuccess) {
+    g_prof_done.push_back(EventPair{t_pending, stop, kind});
+  } else {
+    g_prof_free.push_back(t_pending);
+    if (stop) g_prof_free.push_back(stop);
+  }
+  t_pending = nullptr;
+}
+
+}  // namespace eb
+
+using namespace eb;
+
+extern "C" {
+
+const char* easybalance_version(void) { return "easybalance-mi355x 0.1.0"; }
+
+const char* easybalance_last_error(void) { return g_err; }
+
+int easybalance_route(const eb_model_desc* desc, int32_t layer, int32_t T, const float* x,
+                      const float* gain, const void* Wg, const float* bias, void* a_out,
+                      float* logits_out, int32_t* idx_out, float* w_out, int32_t* counts_out,
+                      void* stream) {
+  int rc = check_desc(desc);
+  if (rc) return rc;
+  if (layer < 0 || layer >= desc->L)
+    return set_error(EB_ERR_INVALID_ARG, "layer=%d outside [0, %d)", layer, desc->L);
+  if (T < 0) return set_error(EB_ERR_INVALID_ARG, "T=%d < 0", T);
+  if (counts_out == nullptr) return set_error(EB_ERR_INVALID_ARG, "counts_out is NULL");
+  if (T > 0 && (x == nullptr || gain == nullptr || Wg == nullptr || bias == nullptr ||
+                a_out == nullptr || logits_out == nullptr || idx_out == nullptr || w_out == nullptr))
+    return set_error(EB_ERR_INVALID_ARG, "a required route pointer is NULL");
+  return hip_status(launch_route(*desc, T, x, gain, Wg, bias, a_out, logits_out, idx_out, w_out,
+                                 counts_out, static_cast<hipStream_t>(stream)),
+                    "route launch");
+}
+
+int easybalance_schedule(int32_t n_pool, const int32_t* pool_ids, const int32_t* counts,
+                         int32_t E, int32_t D, int32_t m, int32_t policy, uint64_t* runset_mask,
+                         int64_t* step_load) {
+  return schedule_impl(n_pool, pool_ids, counts, E, D, m, policy, runset_mask, step_load);
+}
+
+int easybalance_moe_step_workspace_size(const eb_model_desc* desc, int32_t n_run,
+                                        const int32_t* T, size_t* bytes) {
+  int rc = check_desc(desc);
+  if (rc) return rc;
+  if (n_run < 1 || n_run > EB_MAX_RUN || T == nullptr || bytes == nullptr)
+    return set_error(EB_ERR_INVALID_ARG, "bad n_run/T/bytes");
+  for (int i = 0; i < n_run; ++i)
+    if (T[i] < 0) return set_error(EB_ERR_INVALID_ARG, "T[%d] < 0", i);
+  *bytes = ws_layout(*desc, step_shape(*desc, n_run, T), nullptr).total;
+  return EB_OK;
+}
+
+int easybalance_moe_step(const eb_model_desc* desc, int32_t n_run, const eb_work* run,
+                         const void* const* W_gu, const void* const* W_dn, void* ws,
+                         size_t ws_bytes, void* o_out, int32_t* inv_out,
+                         const eb_step_views* views, void* stream) {
+  int rc = check_desc(desc);
+  if (rc) return rc;
+  rc = check_run(*desc, n_run, run, true);
+  if (rc) return rc;
+  const eb_model_desc& d = *desc;
+  std::vector<int32_t> Ts(n_run);
+  for (int i = 0; i < n_run; ++i) Ts[i] = run[i].T;
+  const StepShape sh = step_shape(d, n_run, Ts.data());
+  if (sh.P == 0) return EB_OK;
+  if (W_gu == nullptr || W_dn == nullptr) return set_error(EB_ERR_INVALID_ARG, "W_gu/W_dn is NULL");
+  WeightTable wt;
+  memset(&wt, 0, sizeof(wt));
+  for (int i = 0; i < n_run; ++i) {
+    const int l = run[i].layer;
+    if (run[i].T > 0 && (W_gu[l] == nullptr || W_dn[l] == nullptr))
+      return set_error(EB_ERR_INVALID_ARG, "weights of layer %d are NULL", l);
+  }
+  for (int l = 0; l < d.L; ++l) {
+    wt.gu[l] = W_gu[l];
+    wt.dn[l] = W_dn[l];
+  }
+  if (o_out == nullptr || inv_out == nullptr) return set_error(EB_ERR_INVALID_ARG, "o_out/inv_out is NULL");
+  if (ws == nullptr || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0)
+    return set_error(EB_ERR_INVALID_ARG, "workspace must be non-NULL and 256-byte aligned");
+  const WsLayout L = ws_layout(d, sh, views);
+  if (ws_bytes < L.total)
+    return set_error(EB_ERR_WORKSPACE_TOO_SMALL, "workspace %zu < %zu bytes", ws_bytes, L.total);
+  uint8_t* base = static_cast<uint8_t*>(ws);
+  int32_t* hist = reinterpret_cast<int32_t*>(base + L.hist);
+  int32_t* chunk_base = reinterpret_cast<int32_t*>(base + L.chunk_base);
+  int32_t* offsets = (views && views->offsets) ? views->offsets : reinterpret_cast<int32_t*>(base + L.offsets);
+  int2* tiles = reinterpret_cast<int2*>(base + L.tiles);
+  int32_t* n_tiles = reinterpret_cast<int32_t*>(base + L.n_tiles);
+  int32_t* perm = (views && views->perm) ? views->perm : reinterpret_cast<int32_t*>(base + L.perm);
+  void* a_perm = (views && views->a_perm) ? views->a_perm : base + L.a_perm;
+  void* h = (views && views->h) ? views->h : base + L.h;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+
+  const RunTable rt = make_run_table(d, n_run, run, nullptr);
+  const int eb = d.dtype == EB_DTYPE_BF16 ? 2 : 4;
+  if ((rc = hip_status(launch_perm_count(rt, sh.n_chunks, hist, s), "perm_count"))) return rc;
+  if ((rc = hip_status(launch_perm_scan(rt, sh.n_chunks, hist, chunk_base, offsets, tiles, n_tiles,
+                                        gemm_bm(d.dtype), sh.max_tiles, s),
+                       "perm_scan")))
+    return rc;
+  if ((rc = hip_status(launch_perm_scatter(rt, sh.n_chunks, eb, chunk_base, perm, inv_out, a_perm, s),
+                       "perm_scatter")))
+    return rc;
+  GroupedProblem gp;
+  gp.H = d.H;
+  gp.F = d.F;
+  gp.E = d.E;
+  gp.S = d.S;
+  gp.P = (int32_t)sh.P;
+  gp.offsets = offsets;
+  gp.tiles = tiles;
+  gp.n_tiles = n_tiles;
+  gp.max_tiles = sh.max_tiles;
+  if ((rc = hip_status(launch_gateup(d.dtype, gp, wt, a_perm, h, s), "gate/up GEMM"))) return rc;
+  return hip_status(launch_down(d.dtype, gp, wt, h, o_out, s), "down GEMM");
+}
+
+int easybalance_combine(const eb_model_desc* desc, int32_t n_run, const eb_work* run,
+                        float* const* x_inout, const void* o, const int32_t* inv, void* stream) {
+  int rc = check_desc(desc);
+  if (rc) return rc;
+  rc = check_run(*desc, n_run, run, false);
+  if (rc) return rc;
+  if (x_inout == nullptr) return set_error(EB_ERR_INVALID_ARG, "x_inout is NULL");
+  long long tokens = 0;
+  for (int i = 0; i < n_run; ++i) {
+    if (run[i].T > 0 && x_inout[i] == nullptr)
+      return set_error(EB_ERR_INVALID_ARG, "x_inout[%d] is NULL", i);
+    tokens += run[i].T;
+  }
+  if (tokens == 0) return EB_OK;
+  if (o == nullptr || inv == nullptr) return set_error(EB_ERR_INVALID_ARG, "o/inv is NULL");
+  const RunTable rt = make_run_table(*desc, n_run, run, x_inout);
+  return hip_status(launch_combine(rt, (int)tokens, desc->dtype, o, inv,
+                                   static_cast<hipStream_t>(stream)),
+                    "combine");
+}
+
+int easybalance_profile_begin(void) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  for (auto& p : g_prof_done) {
+    g_prof_free.push_back(p.start);
+    g_prof_free.push_back(p.stop);
+  }
+  g_prof_done.clear();
+  g_prof_on.store(true);
+  return EB_OK;
+}
+
+int easybalance_profile_end(double* ms_out, int64_t* launches_out) {
+  g_prof_on.store(false);
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  double ms[EB_NUM_KERNELS] = {0};
+  int64_t n[EB_NUM_KERNELS] = {0};
+  int rc = EB_OK;
+  for (auto& p : g_prof_done) {
+    float t = 0.f;
+    hipError_t e = hipEventSynchronize(p.stop);
+    if (e == hipSuccess) e = hipEventElapsedTime(&t, p.start, p.stop);
+    if (e != hipSuccess && rc == EB_OK) rc = hip_status(e, "profile events");
+    ms[p.kind] += t;
+    n[p.kind] += 1;
+    g_prof_free.push_back(p.start);
+    g_prof_free.push_back(p.stop);
+  }
+  g_prof_done.clear();
+  if (ms_out) memcpy(ms_out, ms, sizeof(ms));
+  if (launches_out) memcpy(launches_out, n, sizeof(n));
+  return rc;
+}
+
+}  // extern "C"

@@ -1,0 +1,226 @@
+// Stable grouping of a step's (token, expert) pairs by key (layer, expert slot).
+//
+// On an EP group this is the dispatch all-to-all (Section 2.2); with several
+// micro-batches at different layers in one step (Section 4.1) the key carries
+// the layer, so one grouped GEMM launch covers every (layer, expert) group.
+//
+//   perm_count_kernel    per 256-token chunk: routed pairs per expert (LDS atomics)
+//   perm_scan_kernel     one workgroup: per-key totals, offsets, per-chunk bases,
+//                        and the GEMM tile list (key, first row) of BM-row blocks
+//   perm_scatter_kernel  per chunk: stable rank of each pair inside its key from
+//                        per-wavefront 64-bit expert masks (popcount of the lanes
+//                        below), then inv/perm and the activation-row copies
+//
+// Pair q = (tok_base[rho] + t) * (k+S) + r; key = layer*(E+S) + slot expert.
+// All results are integers fixed by the inputs (no order-dependent atomics).
+#include "eb_internal.h"
+#include "eb_numeric.h"
+
+namespace eb {
+namespace {
+
+constexpr int kScanThreads = 1024;
+
+__device__ __forceinline__ int clamp_expert(int e, int E) { return e < 0 ? 0 : (e >= E ? E - 1 : e); }
+
+__global__ __launch_bounds__(kPermChunk) void perm_count_kernel(RunTable rt, int32_t* __restrict__ hist) {
+  __shared__ int cnt[1024];
+  const int b = blockIdx.x;
+  for (int e = threadIdx.x; e < rt.E; e += blockDim.x) cnt[e] = 0;
+  __syncthreads();
+  const int rho = find_entry(rt.chunk_base, rt.n, b);
+  const int T = rt.tok_base[rho + 1] - rt.tok_base[rho];
+  const int t = (b - rt.chunk_base[rho]) * kPermChunk + threadIdx.x;
+  if (t < T) {
+    const int32_t* ix = rt.idx[rho] + (size_t)t * rt.k;
+    for (int r = 0; r < rt.k; ++r) atomicAdd(&cnt[clamp_expert(ix[r], rt.E)], 1);
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < rt.E; e += blockDim.x) hist[(size_t)b * rt.E + e] = cnt[e];
+}
+
+// Block-wide exclusive scan of one value per thread (1024 threads); returns
+// the exclusive prefix, writes the total to *total.
+__device__ int block_exclusive_scan(int v, int* sm, int* total) {
+  const int tid = threadIdx.x;
+  sm[tid] = v;
+  __syncthreads();
+  for (int off = 1; off < kScanThreads; off <<= 1) {
+    const int add = tid >= off ? sm[tid - off] : 0;
+    __syncthreads();
+    sm[tid] += add;
+    __syncthreads();
+  }
+  const int incl = sm[tid];
+  *total = sm[kScanThreads - 1];
+  __syncthreads();
+  return incl - v;
+}
+
+// offsets: [L*(E+S)+1]; chunk_base: [n_chunks][E+S]; tiles: [max_tiles].
+__global__ __launch_bounds__(kScanThreads) void perm_scan_kernel(
+    RunTable rt, int n_chunks, const int32_t* __restrict__ hist, int32_t* __restrict__ chunk_base,
+    int32_t* __restrict__ offsets, int2* __restrict__ tiles, int32_t* __restrict__ n_tiles, int bm,
+    int max_tiles) {
+  extern __shared__ int smem[];  // running[n_keys] | scan[kScanThreads]
+  const int ES = rt.E + rt.S;
+  const int n_keys = rt.L * ES;
+  int* running = smem;
+  int* scan = smem + n_keys;
+  const int tid = threadIdx.x;
+
+  // 1) per-key totals into running[]
+  for (int i = tid; i < n_keys; i += kScanThreads) running[i] = 0;
+  __syncthreads();
+  for (int c = tid; c < ES; c += kScanThreads) {
+    for (int b = 0; b < n_chunks; ++b) {
+      const int rho = find_entry(rt.chunk_base, rt.n, b);
+      const int T = rt.tok_base[rho + 1] - rt.tok_base[rho];
+      const int t0 = (b - rt.chunk_base[rho]) * kPermChunk;
+      const int in_chunk = min(kPermChunk, T - t0);
+      const int v = c < rt.E ? hist[(size_t)b * rt.E + c] : in_chunk;
+      running[rt.layer[rho] * ES + c] += v;
+    }
+  }
+  __syncthreads();
+
+  // 2) exclusive scan over keys -> offsets; thread tid owns a contiguous span
+  const int span = (n_keys + kScanThreads - 1) / kScanThreads;
+  const int k0 = min(tid * span, n_keys), k1 = min(k0 + span, n_keys);
+  int local = 0;
+  for (int i = k0; i < k1; ++i) local += running[i];
+  int total = 0;
+  int base = block_exclusive_scan(local, scan, &total);
+  for (int i = k0; i < k1; ++i) {
+    const int v = running[i];
+    offsets[i] = base;
+    running[i] = base;  // becomes the running cursor of key i
+    base += v;
+  }
+  if (tid == 0) offsets[n_keys] = total;
+  __syncthreads();
+
+  // 3) tile list: ceil(M/bm) row blocks per non-empty key, keys ascending
+  int local_tiles = 0;
+  for (int i = k0; i < k1; ++i) {
+    const int M = offsets[i + 1] - offsets[i];
+    local_tiles += (M + bm - 1) / bm;
+  }
+  int tiles_total = 0;
+  int tb = block_exclusive_scan(local_tiles, scan, &tiles_total);
+  for (int i = k0; i < k1; ++i) {
+    const int r0 = offsets[i], M = offsets[i + 1] - r0;
+    for (int m = 0; m < M; m += bm) {
+      if (tb < max_tiles) tiles[tb] = make_int2(i, r0 + m);
+      ++tb;
+    }
+  }
+  if (tid == 0) *n_tiles = min(tiles_total, max_tiles);
+
+  // 4) per-chunk bases: walk chunks in order, one column per thread
+  for (int c = tid; c < ES; c += kScanThreads) {
+    for (int b = 0; b < n_chunks; ++b) {
+      const int rho = find_entry(rt.chunk_base, rt.n, b);
+      const int T = rt.tok_base[rho + 1] - rt.tok_base[rho];
+      const int t0 = (b - rt.chunk_base[rho]) * kPermChunk;
+      const int in_chunk = min(kPermChunk, T - t0);
+      const int key = rt.layer[rho] * ES + c;
+      chunk_base[(size_t)b * ES + c] = running[key];
+      running[key] += c < rt.E ? hist[(size_t)b * rt.E + c] : in_chunk;
+    }
+  }
+}
+
+// One block per chunk, one token per thread.  `elem_bytes` is 2 (bf16) or 4.
+__global__ __launch_bounds__(kPermChunk) void perm_scatter_kernel(
+    RunTable rt, int elem_bytes, const int32_t* __restrict__ chunk_base,
+    int32_t* __restrict__ perm, int32_t* __restrict__ inv, uint8_t* __restrict__ a_perm) {
+  __shared__ unsigned long long mask[kPermChunk / kWave][1024];
+  __shared__ int pos_s[kPermChunk][kMaxSlots];
+  const int E = rt.E, S = rt.S, k = rt.k, ES = E + S, slots = k + S;
+  const int b = blockIdx.x;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  for (int i = threadIdx.x; i < (kPermChunk / kWave) * E; i += blockDim.x)
+    mask[i / E][i % E] = 0ull;
+  __syncthreads();
+  const int rho = find_entry(rt.chunk_base, rt.n, b);
+  const int T = rt.tok_base[rho + 1] - rt.tok_base[rho];
+  const int t0 = (b - rt.chunk_base[rho]) * kPermChunk;
+  const int t = t0 + threadIdx.x;
+  const bool valid = t < T;
+  int ex[kMaxSlots];
+  if (valid) {
+    const int32_t* ix = rt.idx[rho] + (size_t)t * k;
+    for (int r = 0; r < k; ++r) {
+      ex[r] = clamp_expert(ix[r], E);
+      atomicOr(&mask[wave][ex[r]], 1ull << lane);
+    }
+  }
+  __syncthreads();
+  if (valid) {
+    const unsigned long long below = (1ull << lane) - 1ull;
+    const int32_t* cb = chunk_base + (size_t)b * ES;
+    const size_t q0 = (size_t)(rt.tok_base[rho] + t) * slots;
+    for (int r = 0; r < slots; ++r) {
+      int pos;
+      if (r < k) {
+        const int e = ex[r];
+        int rank = __popcll(mask[wave][e] & below);
+        for (int w2 = 0; w2 < wave; ++w2) rank += __popcll(mask[w2][e]);
+        pos = cb[e] + rank;
+      } else {
+        pos = cb[E + (r - k)] + threadIdx.x;  // every token of the chunk has it
+      }
+      pos_s[threadIdx.x][r] = pos;
+      inv[q0 + r] = pos;
+      if (perm) perm[pos] = (int32_t)(q0 + r);
+    }
+  }
+  __syncthreads();
+  // row copies: each wavefront moves its 64 tokens' rows, 16 bytes per lane
+  const size_t row_bytes = (size_t)rt.H * elem_bytes;
+  const int n16 = (int)(row_bytes / 16);
+  const uint8_t* a_base = static_cast<const uint8_t*>(rt.a[rho]);
+  for (int i = 0; i < kWave; ++i) {
+    const int tl = wave * kWave + i;
+    if (t0 + tl >= T) break;
+    const uint4* src = reinterpret_cast<const uint4*>(a_base + (size_t)(t0 + tl) * row_bytes);
+    for (int c = lane; c < n16; c += kWave) {
+      const uint4 v = src[c];
+      for (int r = 0; r < slots; ++r)
+        reinterpret_cast<uint4*>(a_perm + (size_t)pos_s[tl][r] * row_bytes)[c] = v;
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_perm_count(const RunTable& rt, int n_chunks, int32_t* hist, hipStream_t s) {
+  prof_start(EB_K_PERM_COUNT, s);
+  hipLaunchKernelGGL(perm_count_kernel, dim3(n_chunks), dim3(kPermChunk), 0, s, rt, hist);
+  prof_stop(EB_K_PERM_COUNT, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_perm_scan(const RunTable& rt, int n_chunks, const int32_t* hist,
+                            int32_t* chunk_base, int32_t* offsets, int2* tiles,
+                            int32_t* n_tiles, int bm, int max_tiles, hipStream_t s) {
+  const size_t smem = sizeof(int) * ((size_t)rt.L * (rt.E + rt.S) + kScanThreads);
+  prof_start(EB_K_PERM_SCAN, s);
+  hipLaunchKernelGGL(perm_scan_kernel, dim3(1), dim3(kScanThreads), smem, s, rt, n_chunks, hist,
+                     chunk_base, offsets, tiles, n_tiles, bm, max_tiles);
+  prof_stop(EB_K_PERM_SCAN, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_perm_scatter(const RunTable& rt, int n_chunks, int elem_bytes,
+                               const int32_t* chunk_base, int32_t* perm, int32_t* inv,
+                               void* a_perm, hipStream_t s) {
+  prof_start(EB_K_PERM_SCATTER, s);
+  hipLaunchKernelGGL(perm_scatter_kernel, dim3(n_chunks), dim3(kPermChunk), 0, s, rt, elem_bytes,
+                     chunk_base, perm, inv, static_cast<uint8_t*>(a_perm));
+  prof_stop(EB_K_PERM_SCATTER, s);
+  return hipGetLastError();
+}
+
+}  // namespace eb

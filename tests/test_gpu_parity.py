@@ -1,0 +1,213 @@
+"""GPU parity of every stage of the hot path against the CPU oracle, through
+the C ABI, on seeded inputs at sizes the oracle finishes in seconds (several
+GEMM tiles, ragged tails, empty entries).
+
+Contract (teacher-forced where floating point decides an integer):
+* idx, counts, perm, inv, offsets, a_perm, schedules: bit-exact;
+* activations (a, z, w, h, o, x): max-abs error <= 1e-5 * max|ref| (fp32
+  stacks) or 1e-2 * max|ref| (bf16 stacks).
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import metrics as ometrics
+from oracle import model as omodel
+from oracle import permute as operm
+from oracle import sched as osched
+from oracle.numerics import cast_fn
+from synth import CONFIGS, gen, mini
+from synth.device import DeviceInputs, fill_
+
+from gpu_helpers import assert_close, host_weights, log, make_stack, to_np
+
+pytestmark = pytest.mark.gpu
+
+MINIS = [CONFIGS[0]] + [mini(c) for c in CONFIGS[1:]]
+IDS = [c.name for c in MINIS]
+
+
+def _binding():
+    from paper_2608_07964_amd import binding as B
+    B.lib()
+    return B
+
+
+def test_device_generator_bit_exact(device):
+    cfg = MINIS[1]
+    for kind, index, dt in [(gen.KIND_X, 0, torch.float32), (gen.KIND_GU, 2, torch.bfloat16),
+                            (gen.KIND_WG, 1, torch.float32), (gen.KIND_DN, 0, torch.bfloat16)]:
+        t = fill_(torch.empty(100003, dtype=dt, device=device), cfg, kind, index, i0=777)
+        ref = gen.normal_f32(gen.stream_key(cfg.seed, kind, index), 777, 100003, gen.sigma_of(kind, cfg.H))
+        if dt == torch.bfloat16:
+            got = t.view(torch.int16).cpu().numpy().view(np.uint16)
+            assert np.array_equal(got, gen.f32_to_bf16_bits(ref))
+        else:
+            assert np.array_equal(t.cpu().numpy(), ref)
+
+
+@pytest.mark.parametrize("cfg", MINIS, ids=IDS)
+def test_route_stage(cfg, device):
+    B = _binding()
+    log(f"route parity {cfg.name}")
+    inp = DeviceInputs(cfg, device, weights=False)
+    P = host_weights(cfg)
+    desc = B.make_desc(cfg.L, cfg.H, cfg.F, cfg.E, cfg.k, cfg.S, cfg.D, cfg.dtype, cfg.eps)
+    tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    for T, l, j in [(cfg.T, cfg.L - 1, 1), (1, 0, 0), (cfg.T - 3, 0, cfg.N - 1)]:
+        x = inp.x0[j, :T].clone()
+        a = torch.empty(T, cfg.H, dtype=tdt, device=device)
+        z = torch.empty(T, cfg.E, dtype=torch.float32, device=device)
+        idx = torch.empty(T, cfg.k, dtype=torch.int32, device=device)
+        w = torch.empty(T, cfg.k, dtype=torch.float32, device=device)
+        counts = torch.full((cfg.E,), 12345, dtype=torch.int32, device=device)
+        B.easybalance_route(desc, l, T, x, inp.g[l], inp.Wg[l], inp.bias[l], a, z, idx, w, counts)
+        torch.cuda.synchronize()
+        xh = to_np(x)
+        a_ref = omodel.rmsnorm_cast(xh, P.gain(l), cfg.eps, cast_fn(cfg.dtype))
+        assert_close(to_np(a), a_ref, cfg.dtype, "a")
+        zg = to_np(z)
+        assert_close(zg, omodel.router_logits(to_np(a), P.router(l), P.bias(l)), cfg.dtype, "logits")
+        idx_ref = omodel.topk_indices(zg, cfg.k)                      # teacher-forced on GPU logits
+        assert np.array_equal(idx.cpu().numpy(), idx_ref)
+        assert_close(to_np(w), omodel.gate_weights(zg, idx_ref, cfg.norm_topk), cfg.dtype, "w")
+        assert np.array_equal(counts.cpu().numpy(), omodel.expert_counts(idx_ref, cfg.E))
+
+
+def _route_entry(B, desc, cfg, inp, j, l, T, device):
+    tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    x = inp.x0[j, :T].clone()
+    bufs = dict(x=x, a=torch.zeros(max(T, 1), cfg.H, dtype=tdt, device=device),
+                z=torch.empty(max(T, 1), cfg.E, dtype=torch.float32, device=device),
+                idx=torch.empty(max(T, 1), cfg.k, dtype=torch.int32, device=device),
+                w=torch.empty(max(T, 1), cfg.k, dtype=torch.float32, device=device),
+                counts=torch.empty(cfg.E, dtype=torch.int32, device=device), T=T, l=l, j=j)
+    B.easybalance_route(desc, l, T, x, inp.g[l], inp.Wg[l], inp.bias[l], bufs["a"], bufs["z"],
+                        bufs["idx"], bufs["w"], bufs["counts"])
+    return bufs
+
+
+@pytest.mark.parametrize("cfg", MINIS, ids=IDS)
+def test_moe_step_and_combine_stage(cfg, device):
+    """One cross-layer step with entries at different layers, ragged and empty
+    token counts; every stage checked against the oracle on the GPU's inputs."""
+    B = _binding()
+    log(f"step parity {cfg.name}")
+    inp = DeviceInputs(cfg, device)
+    P = host_weights(cfg)
+    cast = cast_fn(cfg.dtype)
+    desc = B.make_desc(cfg.L, cfg.H, cfg.F, cfg.E, cfg.k, cfg.S, cfg.D, cfg.dtype, cfg.eps)
+    L = cfg.L
+    plan = [(0, min(1, L - 1), cfg.T), (1, L - 1, cfg.T - 37), (2 % cfg.N, 0, 0),
+            (cfg.N - 1, 0, 5 if cfg.T > 5 else 1)]
+    ents = [_route_entry(B, desc, cfg, inp, j, l, T, device) for j, l, T in plan]
+    run = B.work_array((e["j"], e["l"], e["T"], e["a"], e["idx"], e["w"]) for e in ents)
+    Ts = [e["T"] for e in ents]
+    slots = cfg.k + cfg.S
+    Ptot = sum(Ts) * slots
+    ws_bytes = B.easybalance_moe_step_workspace_size(desc, Ts)
+    ws = torch.empty(ws_bytes + 256, dtype=torch.uint8, device=device)
+    wsp = ws.data_ptr() + (-ws.data_ptr()) % 256
+    tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    o = torch.empty(Ptot, cfg.H, dtype=tdt, device=device)
+    inv = torch.empty(Ptot, dtype=torch.int32, device=device)
+    views = dict(a_perm=torch.empty(Ptot, cfg.H, dtype=tdt, device=device),
+                 h=torch.empty(Ptot, cfg.F, dtype=tdt, device=device),
+                 perm=torch.empty(Ptot, dtype=torch.int32, device=device),
+                 offsets=torch.empty(L * (cfg.E + cfg.S) + 1, dtype=torch.int32, device=device))
+    B.easybalance_moe_step(desc, run, len(ents), inp.W_gu, inp.W_dn, wsp, ws_bytes, o, inv, views)
+    x_before = [to_np(e["x"]) for e in ents]
+    B.easybalance_combine(desc, run, len(ents), [e["x"] for e in ents], o, inv)
+    torch.cuda.synchronize()
+
+    # permutation: bit-exact against the stable sort of the GPU's own routing
+    run_np = [(e["l"], e["idx"].cpu().numpy()[:e["T"]]) for e in ents]
+    keys = operm.step_keys(run_np, cfg.E, cfg.S)
+    perm_ref, inv_ref, off_ref = operm.stable_permutation(keys, L * (cfg.E + cfg.S))
+    assert np.array_equal(inv.cpu().numpy(), inv_ref)
+    assert np.array_equal(views["perm"].cpu().numpy(), perm_ref)
+    assert np.array_equal(views["offsets"].cpu().numpy(), off_ref)
+    # grouped activation rows are exact copies
+    src = operm.source_rows(run_np, cfg.S)
+    a_all = [to_np(e["a"]) for e in ents]
+    a_perm = to_np(views["a_perm"])
+    assert np.array_equal(a_perm[inv_ref], np.stack([a_all[r][t] for r, t in src]) if len(src) else a_perm[:0])
+    # expert FFN per group, teacher-forced on the GPU's a_perm (h) and h (o)
+    h_gpu, o_gpu = to_np(views["h"]), to_np(o)
+    h_ref = np.zeros_like(h_gpu)
+    o_ref = np.zeros_like(o_gpu)
+    for key in range(L * (cfg.E + cfg.S)):
+        r0, r1 = off_ref[key], off_ref[key + 1]
+        if r0 == r1:
+            continue
+        l, e = divmod(key, cfg.E + cfg.S)
+        Wg_, Wu_ = P.gate_up(l, e)
+        Wd_ = P.down(l, e)
+        h_ref[r0:r1], _ = omodel.expert_ffn(a_perm[r0:r1], Wg_, Wu_, Wd_, cast)
+        o_ref[r0:r1] = cast(h_gpu[r0:r1] @ np.asarray(Wd_, np.float64).T)
+    assert_close(h_gpu, h_ref, cfg.dtype, "h")
+    assert_close(o_gpu, o_ref, cfg.dtype, "o")
+    # combine: x + sum_r w_r o_r + sum_s o_s, on the GPU's o
+    q = 0
+    for e, xb in zip(ents, x_before):
+        T = e["T"]
+        if T == 0:
+            continue
+        rows = inv_ref[q:q + T * slots].reshape(T, slots)
+        q += T * slots
+        want = omodel.combine(xb, o_gpu[rows[:, :cfg.k]], to_np(e["w"])[:T],
+                              o_gpu[rows[:, cfg.k:]] if cfg.S else None)
+        assert_close(to_np(e["x"]), want, "f32", "x after combine")
+
+
+def test_tiny_fp32_end_to_end_free_running(device):
+    """The fp32 stack through the whole EB pass against the oracle's plain
+    layer-by-layer run: routing, schedule and hidden states."""
+    cfg = CONFIGS[0]
+    log("end-to-end tiny fp32")
+    st, inp = make_stack(cfg, device)
+    steps = st.run("maxutil", m=cfg.m)
+    torch.cuda.synchronize()
+    P = host_weights(cfg)
+    ref = omodel.run_plain(gen.x_all(cfg), P, L=cfg.L, E=cfg.E, k=cfg.k, S=cfg.S, D=cfg.D,
+                           eps=cfg.eps, dtype=cfg.dtype)
+    # the seed gives no near-ties: the k-th and (k+1)-th logits are well apart
+    for j in range(cfg.N):
+        for l in range(cfg.L):
+            a = omodel.rmsnorm_cast(ref.x[l, j], P.gain(l), cfg.eps, cast_fn(cfg.dtype))
+            z = np.sort(omodel.router_logits(a, P.router(l), P.bias(l)), axis=1)[:, ::-1]
+            assert np.min(z[:, cfg.k - 1] - z[:, cfg.k]) > 1e-4
+    assert np.array_equal(st.layer_loads, ref.loads)
+    assert [s.runset for s in steps] == osched.run_algorithm1(ref.loads, cfg.m, osched.MAXUTIL)
+    assert_close(to_np(st.x), ref.x[cfg.L], cfg.dtype, "x final")
+
+
+@pytest.mark.parametrize("cfg", MINIS, ids=IDS)
+def test_schedule_invariance_and_replay(cfg, device):
+    """Cross-layer joint execution is lossless (Section 4.1): the EB schedule
+    and the per-layer lock-step schedule give bit-identical hidden states, and
+    every executed schedule is the oracle's replay of Algorithm 1 on the loads
+    the GPU observed."""
+    log(f"invariance {cfg.name}")
+    inp = DeviceInputs(cfg, device)
+    results = {}
+    for policy, m in [("lockstep", None), ("maxutil", cfg.m), ("maxutil", 1), ("cumutil", cfg.m),
+                      ("diffpeak", cfg.m)]:
+        st, _ = make_stack(cfg, device, inputs=inp)
+        steps = st.run(policy, m=m)
+        torch.cuda.synchronize()
+        results[(policy, m)] = (st.x.clone(), steps, st.layer_loads.copy())
+        if policy != "lockstep":
+            pol = {"maxutil": osched.MAXUTIL, "cumutil": osched.CUMUTIL, "diffpeak": osched.DIFFPEAK}[policy]
+            assert [s.runset for s in steps] == osched.run_algorithm1(st.layer_loads, m, pol)
+            for s in steps:
+                assert np.array_equal(s.load, ometrics.step_workload(st.layer_loads, s.runset))
+    x_ls, steps_ls, loads_ls = results[("lockstep", None)]
+    assert [s.runset for s in steps_ls] == osched.lockstep_steps(cfg.N, cfg.L)
+    for key, (x, steps, loads) in results.items():
+        assert np.array_equal(loads, loads_ls), key
+        assert torch.equal(x, x_ls), f"{key}: hidden states differ from lock-step"
+    # worst-case safety on the observed loads
+    eb = results[("maxutil", cfg.m)][1]
+    assert (ometrics.utilization(loads_ls, [s.runset for s in eb])
+            >= ometrics.utilization(loads_ls, osched.separate_steps(cfg.N, cfg.L)))
