@@ -1,0 +1,228 @@
+#!/usr/bin/env python3
+"""Benchmark of the EasyBalance hot path on one MI355X.
+
+One step = one full pass of Algorithm 1 over one batch: every micro-batch of
+the stack through every MoE layer (routing, MaxUtil scheduling, grouped
+expert FFN of each step's RunSet, weighted combine), starting from the same
+synthetic residual stream each time.  Inputs and weights are generated in HBM
+before timing.  Prints ONE JSON line:
+
+  value      expert-FFN TFLOP/s of the whole pass: 6*H*F FLOP per routed or
+             shared (token, expert) pair, over the wall time of the pass
+  load       max/mean virtual-device load (and idle fraction) of the executed
+             schedule vs the per-layer lock-step baseline and vs no combination
+  roofline   the grouped gate/up GEMM (the dominant kernel), timed with HIP
+             events on its own stream over the timed region
+  cpu_baseline  the CPU oracle timed on a bounded sample of the same workload
+
+Only one GPU: --gpus N with N > 1 exits with an error.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_FP32_VALU_TFLOPS = 157.3  # MI355X fp32 vector
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def gemm_source_hash() -> str:
+    with open(os.path.join(ROOT, "paper_2608_07964_amd", "csrc", "gemm.hip"), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic(config: str):
+    """HBM bytes per gate/up launch from the committed rocprofv3 counter summary,
+    if it was taken on the current kernel source (else None)."""
+    path = os.path.join(ROOT, "profiles", f"gateup_traffic_{config}.json")
+    try:
+        with open(path) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("gemm_source_sha256_16") != gemm_source_hash():
+        return None
+    return t.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(cfg, budget_s: float) -> dict:
+    """The oracle (float64 NumPy) on whole (micro-batch, layer-0) MoE layers of
+    the same stack, as many as fit in ~budget_s; weights generated beforehand."""
+    import numpy as np
+    import threadpoolctl
+
+    from oracle import model as omodel
+    from synth import gen
+
+    bias = gen.router_bias(cfg)
+    t_gen = time.perf_counter()
+    gu = {e: gen.expert_gate_up(cfg, 0, e) for e in range(cfg.E + cfg.S)}
+    dn = {e: gen.expert_down(cfg, 0, e) for e in range(cfg.E + cfg.S)}
+    Wr = gen.router_weight(cfg, 0)
+    log(f"cpu baseline: generated layer-0 weights in {time.perf_counter() - t_gen:.1f}s")
+    P = omodel.Weights(gain=lambda l: gen.rms_gain(cfg), router=lambda l: Wr,
+                       bias=lambda l: bias[l], gate_up=lambda l, e: gu[e], down=lambda l, e: dn[e])
+    info = threadpoolctl.threadpool_info()
+    cores = max([i.get("num_threads", 1) for i in info if i.get("user_api") == "blas"] or [1])
+    done, t_total = 0, 0.0
+    for j in range(cfg.N):
+        x = gen.x_rows(cfg, j, 0, cfg.T).astype(np.float64)
+        t0 = time.perf_counter()
+        omodel.moe_layer(x, 0, P, E=cfg.E, k=cfg.k, S=cfg.S, eps=cfg.eps, dtype=cfg.dtype)
+        t_total += time.perf_counter() - t0
+        done += 1
+        if t_total >= budget_s:
+            break
+    flops = done * cfg.T * (cfg.k + cfg.S) * cfg.ffn_flop_per_pair
+    return {"value": flops / t_total / 1e12, "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+            "sample": (f"oracle MoE layer 0 of micro-batches 0..{done - 1} ({cfg.T} tokens each, "
+                       f"{cfg.name}), float64 NumPy/OpenBLAS, {t_total:.1f}s; expert-FFN FLOP "
+                       f"counted as on the GPU")}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", default="mixtral_bf16")
+    ap.add_argument("--policy", default="maxutil", choices=["maxutil", "cumutil", "diffpeak", "lockstep"])
+    ap.add_argument("--m", type=int, default=None, help="minimum combination size (default 0.75 N)")
+    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-lockstep", action="store_true", help="skip the lock-step comparison pass")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU "
+              "expert-parallel path is not part of this build", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2608_07964_amd import binding as B
+    from paper_2608_07964_amd import metrics
+    from paper_2608_07964_amd.driver import Stack
+    from synth import BY_NAME
+    from synth.device import DeviceInputs
+
+    cfg = BY_NAME[args.config]
+    m = args.m if args.m is not None else cfg.m
+    B.lib()
+    dev = "cuda:0"
+    t0 = time.perf_counter()
+    inp = DeviceInputs(cfg, dev)
+    torch.cuda.synchronize()
+    log(f"{cfg.name}: inputs generated in HBM in {time.perf_counter() - t0:.2f}s "
+        f"({inp.weight_bytes() / 1e9:.1f} GB of expert weights)")
+    st = Stack(L=cfg.L, H=cfg.H, F=cfg.F, E=cfg.E, k=cfg.k, S=cfg.S, D=cfg.D, N=cfg.N, T=cfg.T,
+               dtype=cfg.dtype, x=inp.x0.clone(), gain=inp.g, Wg=inp.Wg, bias=inp.bias,
+               W_gu=inp.W_gu, W_dn=inp.W_dn, eps=cfg.eps, norm_topk=cfg.norm_topk, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def one_pass(policy, record=False):
+        st.x.copy_(inp.x0)
+        return st.run(policy, m=m, record=record, stream=stream)
+
+    flop_pass = cfg.total_ffn_flop
+    pairs_pass = cfg.N * cfg.T * (cfg.k + cfg.S) * cfg.L
+
+    def timed(policy, K, W, profile):
+        for _ in range(W):
+            one_pass(policy)
+        torch.cuda.synchronize()
+        if profile:
+            B.easybalance_profile_begin()
+        t = time.perf_counter()
+        for _ in range(K):
+            one_pass(policy)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t
+        prof = B.easybalance_profile_end() if profile else None
+        return dt, prof
+
+    dt, prof = timed(args.policy, args.steps, args.warmup, True)
+    ms_step = dt / args.steps * 1e3
+    value = flop_pass * args.steps / dt / 1e12
+    log(f"{args.policy}: {ms_step:.3f} ms/pass, {value:.1f} TFLOP/s")
+
+    steps = one_pass(args.policy, record=True)
+    torch.cuda.synchronize()
+    layer_loads = st.layer_loads.copy()
+    load = {
+        "schedule": metrics.summary([s.load for s in steps]),
+        "per_layer_baseline": metrics.summary(metrics.lockstep_loads(layer_loads)),
+        "no_combination": metrics.summary(metrics.separate_loads(layer_loads)),
+    }
+    extra = {}
+    if not args.no_lockstep and args.policy != "lockstep":
+        dt_ls, _ = timed("lockstep", args.steps, 1, False)
+        extra["lockstep_tflops"] = flop_pass * args.steps / dt_ls / 1e12
+        extra["lockstep_ms_per_step"] = dt_ls / args.steps * 1e3
+
+    # roofline of the grouped gate/up GEMM over the timed region
+    gu_ms, gu_n = prof["gateup"]
+    dn_ms, dn_n = prof["down"]
+    eb = 2 if cfg.dtype == "bf16" else 4
+    gu_flop = 4 * cfg.H * cfg.F * pairs_pass * args.steps
+    groups = sum(s.groups for s in steps) * args.steps
+    gu_bytes = (groups * 2 * cfg.F * cfg.H * eb
+                + pairs_pass * args.steps * (cfg.H + cfg.F) * eb)     # weights + A in + h out
+    t_gu = gu_ms / 1e3
+    peak_flops = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_FP32_VALU_TFLOPS
+    compute_s = gu_flop / (peak_flops * 1e12)
+    memory_s = gu_bytes / (PEAK_HBM_GBS * 1e9)
+    traffic = measured_traffic(cfg.name)
+    if compute_s >= memory_s:
+        ach = gu_flop / t_gu / 1e12
+        roof = {"bound": "mfma" if cfg.dtype == "bf16" else "alu", "achieved": ach,
+                "peak": peak_flops, "unit": "TFLOP/s", "frac": ach / peak_flops, "traffic": traffic}
+    else:
+        ach = gu_bytes / t_gu / 1e9
+        roof = {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": ach / PEAK_HBM_GBS, "traffic": traffic}
+    roof.update({"kernel": "grouped_gemm_bf16<gate/up+SwiGLU>" if cfg.dtype == "bf16" else "grouped_gemm_f32<gate/up>",
+                 "launches": gu_n, "avg_launch_ms": gu_ms / max(gu_n, 1),
+                 "algorithmic_flop_per_launch": gu_flop / max(gu_n, 1),
+                 "algorithmic_bytes_per_launch": gu_bytes / max(gu_n, 1),
+                 "time_at_mfma_peak_ms": compute_s * 1e3 / max(gu_n, 1),
+                 "time_at_hbm_peak_ms": memory_s * 1e3 / max(gu_n, 1)})
+    kernels = {name: {"ms_per_step": ms / args.steps, "launches_per_step": n / args.steps}
+               for name, (ms, n) in prof.items()}
+    ffn_tflops = 6 * cfg.H * cfg.F * pairs_pass * args.steps / ((gu_ms + dn_ms) / 1e3) / 1e12
+
+    out = {
+        "metric": "expert-FFN TFLOP/s (1 GPU) + max/mean virtual-device load vs per-layer base",
+        "value": value, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if cfg.dtype == "bf16" else "f32", "data": "synthetic",
+        "config": {"workload": cfg.name, "L": cfg.L, "H": cfg.H, "F": cfg.F, "E": cfg.E, "k": cfg.k,
+                   "S": cfg.S, "D": cfg.D, "N": cfg.N, "T": cfg.T, "m": m, "policy": args.policy,
+                   "tokens_per_step": cfg.N * cfg.T, "ffn_flop_per_step": flop_pass},
+        "load": load,
+        "steps_per_pass": len(steps),
+        "ffn_kernels_tflops": ffn_tflops,
+        "kernels": kernels,
+        "roofline": roof,
+        **extra,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -27,8 +27,8 @@
  *    type (EB_DTYPE_F32 or EB_DTYPE_BF16, bf16 as raw 16-bit patterns);
  *    accumulation is always fp32.
  *  - Shape limits (EB_ERR_UNSUPPORTED otherwise): H % 256 == 0,
- *    F % 128 == 0, 1 <= k <= E, E + S <= 1024, E % D == 0, L <= EB_MAX_LAYERS,
- *    L * (E + S) <= 15360.
+ *    F % 128 == 0, 1 <= k <= E, E + S <= 1024, k + S <= 16, E % D == 0,
+ *    L <= EB_MAX_LAYERS, L * (E + S) <= 15360.
  */
 #ifndef EASYBALANCE_H
 #define EASYBALANCE_H
@@ -68,7 +68,8 @@ extern "C" {
 #define EB_K_GATEUP 6
 #define EB_K_DOWN 7
 #define EB_K_COMBINE 8
-#define EB_NUM_KERNELS 9
+#define EB_K_PERM_GATHER 9
+#define EB_NUM_KERNELS 10
 
 /* Model shape.  L MoE layers, hidden H, expert FFN size F, E routed experts
  * with top-k routing, S always-on shared experts, D virtual EP devices.

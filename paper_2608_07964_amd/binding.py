@@ -26,7 +26,7 @@ EB_POLICY_MAXUTIL, EB_POLICY_CUMUTIL, EB_POLICY_DIFFPEAK = 0, 1, 2
 EB_MAX_POOL = 64
 EB_MAXUTIL_MAX_POOL = 20
 KERNEL_NAMES = ["route_norm", "route_logits", "route_topk", "perm_count", "perm_scan",
-                "perm_scatter", "gateup", "down", "combine"]
+                "perm_scatter", "gateup", "down", "combine", "perm_gather"]
 EB_NUM_KERNELS = len(KERNEL_NAMES)
 
 EXPORTS = ["easybalance_version", "easybalance_last_error", "easybalance_route",

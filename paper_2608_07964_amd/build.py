@@ -22,6 +22,8 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libeasybalance.so")
 SYNTH_SRC = os.path.join(ROOT, "synth", "fill.hip")
 SYNTH_LIB = os.path.join(ROOT, "synth", "libebsynth.so")
+SYNTH_HOST_SRC = os.path.join(ROOT, "synth", "gen_host.c")
+SYNTH_HOST_LIB = os.path.join(ROOT, "synth", "libsynthhost.so")
 
 SOURCES = ["api.cpp", "schedule.cpp", "route.hip", "permute.hip", "gemm.hip", "combine.hip"]
 
@@ -65,9 +67,14 @@ def build(verbose: bool = True) -> list[str]:
     tmp = SYNTH_LIB + ".tmp"
     _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", synth_obj, "-o", tmp])
     os.replace(tmp, SYNTH_LIB)
+    # host generator: plain C, IEEE fp32 (no contraction, no fast-math)
+    tmp = SYNTH_HOST_LIB + ".tmp"
+    _run(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-ffp-contract=off", SYNTH_HOST_SRC,
+          "-o", tmp])
+    os.replace(tmp, SYNTH_HOST_LIB)
     if verbose:
-        print(f"built {LIB} and {SYNTH_LIB} for {ARCH}")
-    return [LIB, SYNTH_LIB]
+        print(f"built {LIB}, {SYNTH_LIB} ({ARCH}) and {SYNTH_HOST_LIB}")
+    return [LIB, SYNTH_LIB, SYNTH_HOST_LIB]
 
 
 if __name__ == "__main__":

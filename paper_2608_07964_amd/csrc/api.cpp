@@ -63,7 +63,7 @@ StepShape step_shape(const eb_model_desc& d, int n_run, const int32_t* T) {
 }
 
 struct WsLayout {
-  size_t hist, chunk_base, offsets, tiles, n_tiles, perm, a_perm, h, total;
+  size_t hist, chunk_base, offsets, tiles, n_tiles, groups, n_groups, perm, a_perm, h, total;
 };
 
 WsLayout ws_layout(const eb_model_desc& d, const StepShape& s, const eb_step_views* v) {
@@ -80,6 +80,8 @@ WsLayout ws_layout(const eb_model_desc& d, const StepShape& s, const eb_step_vie
   w.offsets = (v && v->offsets) ? 0 : take(sizeof(int32_t) * ((size_t)d.L * (d.E + d.S) + 1));
   w.tiles = take(sizeof(int2) * (size_t)(s.max_tiles > 0 ? s.max_tiles : 1));
   w.n_tiles = take(sizeof(int32_t));
+  w.groups = take(sizeof(int4) * (size_t)d.L * (d.E + d.S));
+  w.n_groups = take(sizeof(int32_t));
   w.perm = (v && v->perm) ? 0 : take(sizeof(int32_t) * (size_t)s.P);
   w.a_perm = (v && v->a_perm) ? 0 : take(eb * (size_t)s.P * d.H);
   w.h = (v && v->h) ? 0 : take(eb * (size_t)s.P * d.F);
@@ -275,6 +277,8 @@ int easybalance_moe_step(const eb_model_desc* desc, int32_t n_run, const eb_work
   int32_t* offsets = (views && views->offsets) ? views->offsets : reinterpret_cast<int32_t*>(base + L.offsets);
   int2* tiles = reinterpret_cast<int2*>(base + L.tiles);
   int32_t* n_tiles = reinterpret_cast<int32_t*>(base + L.n_tiles);
+  int4* groups = reinterpret_cast<int4*>(base + L.groups);
+  int32_t* n_groups = reinterpret_cast<int32_t*>(base + L.n_groups);
   int32_t* perm = (views && views->perm) ? views->perm : reinterpret_cast<int32_t*>(base + L.perm);
   void* a_perm = (views && views->a_perm) ? views->a_perm : base + L.a_perm;
   void* h = (views && views->h) ? views->h : base + L.h;
@@ -284,10 +288,10 @@ int easybalance_moe_step(const eb_model_desc* desc, int32_t n_run, const eb_work
   const int eb = d.dtype == EB_DTYPE_BF16 ? 2 : 4;
   if ((rc = hip_status(launch_perm_count(rt, sh.n_chunks, hist, s), "perm_count"))) return rc;
   if ((rc = hip_status(launch_perm_scan(rt, sh.n_chunks, hist, chunk_base, offsets, tiles, n_tiles,
-                                        gemm_bm(d.dtype), sh.max_tiles, s),
+                                        groups, n_groups, gemm_bm(d.dtype), sh.max_tiles, s),
                        "perm_scan")))
     return rc;
-  if ((rc = hip_status(launch_perm_scatter(rt, sh.n_chunks, eb, chunk_base, perm, inv_out, a_perm, s),
+  if ((rc = hip_status(launch_perm_scatter(rt, sh.n_chunks, (int)sh.P, eb, chunk_base, perm, inv_out, a_perm, s),
                        "perm_scatter")))
     return rc;
   GroupedProblem gp;
@@ -299,6 +303,8 @@ int easybalance_moe_step(const eb_model_desc* desc, int32_t n_run, const eb_work
   gp.offsets = offsets;
   gp.tiles = tiles;
   gp.n_tiles = n_tiles;
+  gp.groups = groups;
+  gp.n_groups = n_groups;
   gp.max_tiles = sh.max_tiles;
   if ((rc = hip_status(launch_gateup(d.dtype, gp, wt, a_perm, h, s), "gate/up GEMM"))) return rc;
   return hip_status(launch_down(d.dtype, gp, wt, h, o_out, s), "down GEMM");

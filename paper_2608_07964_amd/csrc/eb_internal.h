@@ -37,7 +37,9 @@ struct GroupedProblem {
   int32_t P;                               // grouped rows
   const int32_t* offsets;                  // [L*(E+S)+1]
   const int2* tiles;                       // [n_tiles] (key, first row)
-  const int32_t* n_tiles;                  // device scalar
+  const int32_t* n_tiles;                  // device scalar: row blocks over all groups
+  const int4* groups;                      // [n_groups] (key, first row, rows, first row block)
+  const int32_t* n_groups;                 // device scalar: non-empty keys
   int32_t max_tiles;                       // grid bound
 };
 
@@ -59,8 +61,9 @@ hipError_t launch_route(const eb_model_desc& d, int T, const float* x, const flo
 hipError_t launch_perm_count(const RunTable& rt, int n_chunks, int32_t* hist, hipStream_t s);
 hipError_t launch_perm_scan(const RunTable& rt, int n_chunks, const int32_t* hist,
                             int32_t* chunk_base, int32_t* offsets, int2* tiles,
-                            int32_t* n_tiles, int bm, int max_tiles, hipStream_t s);
-hipError_t launch_perm_scatter(const RunTable& rt, int n_chunks, int elem_bytes,
+                            int32_t* n_tiles, int4* groups, int32_t* n_groups, int bm,
+                            int max_tiles, hipStream_t s);
+hipError_t launch_perm_scatter(const RunTable& rt, int n_chunks, int P, int elem_bytes,
                                const int32_t* chunk_base, int32_t* perm, int32_t* inv,
                                void* a_perm, hipStream_t s);
 

@@ -21,10 +21,13 @@ __device__ __forceinline__ bf16_t f32_to_bf16(float f) {
 
 template <typename T> struct Elem;
 template <> struct Elem<float> {
+  __device__ static __forceinline__ float round(float v) { return v; }
   __device__ static __forceinline__ float load(const float* p, size_t i) { return p[i]; }
   __device__ static __forceinline__ void store(float* p, size_t i, float v) { p[i] = v; }
 };
 template <> struct Elem<bf16_t> {
+  // the value that storing v and loading it back gives
+  __device__ static __forceinline__ float round(float v) { return bf16_to_f32(f32_to_bf16(v)); }
   __device__ static __forceinline__ float load(const bf16_t* p, size_t i) { return bf16_to_f32(p[i]); }
   __device__ static __forceinline__ void store(bf16_t* p, size_t i, float v) { p[i] = f32_to_bf16(v); }
 };

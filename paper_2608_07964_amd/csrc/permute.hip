@@ -6,10 +6,13 @@
 //
 //   perm_count_kernel    per 256-token chunk: routed pairs per expert (LDS atomics)
 //   perm_scan_kernel     one workgroup: per-key totals, offsets, per-chunk bases,
-//                        and the GEMM tile list (key, first row) of BM-row blocks
+//                        the GEMM tile list (key, first row) of BM-row blocks and
+//                        the list of non-empty groups (key, first row, rows,
+//                        index of its first row block)
 //   perm_scatter_kernel  per chunk: stable rank of each pair inside its key from
 //                        per-wavefront 64-bit expert masks (popcount of the lanes
-//                        below), then inv/perm and the activation-row copies
+//                        below), then inv and perm
+//   gather_rows_kernel   one wavefront per grouped row: a_perm[p] = a of perm[p]
 //
 // Pair q = (tok_base[rho] + t) * (k+S) + r; key = layer*(E+S) + slot expert.
 // All results are integers fixed by the inputs (no order-dependent atomics).
@@ -60,8 +63,8 @@ __device__ int block_exclusive_scan(int v, int* sm, int* total) {
 // offsets: [L*(E+S)+1]; chunk_base: [n_chunks][E+S]; tiles: [max_tiles].
 __global__ __launch_bounds__(kScanThreads) void perm_scan_kernel(
     RunTable rt, int n_chunks, const int32_t* __restrict__ hist, int32_t* __restrict__ chunk_base,
-    int32_t* __restrict__ offsets, int2* __restrict__ tiles, int32_t* __restrict__ n_tiles, int bm,
-    int max_tiles) {
+    int32_t* __restrict__ offsets, int2* __restrict__ tiles, int32_t* __restrict__ n_tiles,
+    int4* __restrict__ groups, int32_t* __restrict__ n_groups, int bm, int max_tiles) {
   extern __shared__ int smem[];  // running[n_keys] | scan[kScanThreads]
   const int ES = rt.E + rt.S;
   const int n_keys = rt.L * ES;
@@ -100,22 +103,28 @@ __global__ __launch_bounds__(kScanThreads) void perm_scan_kernel(
   if (tid == 0) offsets[n_keys] = total;
   __syncthreads();
 
-  // 3) tile list: ceil(M/bm) row blocks per non-empty key, keys ascending
-  int local_tiles = 0;
+  // 3) tile and group lists: ceil(M/bm) row blocks per non-empty key, keys ascending
+  int local_tiles = 0, local_groups = 0;
   for (int i = k0; i < k1; ++i) {
     const int M = offsets[i + 1] - offsets[i];
     local_tiles += (M + bm - 1) / bm;
+    local_groups += M > 0;
   }
-  int tiles_total = 0;
+  int tiles_total = 0, groups_total = 0;
   int tb = block_exclusive_scan(local_tiles, scan, &tiles_total);
+  int gb = block_exclusive_scan(local_groups, scan, &groups_total);
   for (int i = k0; i < k1; ++i) {
     const int r0 = offsets[i], M = offsets[i + 1] - r0;
+    if (M > 0) groups[gb++] = make_int4(i, r0, M, tb);
     for (int m = 0; m < M; m += bm) {
       if (tb < max_tiles) tiles[tb] = make_int2(i, r0 + m);
       ++tb;
     }
   }
-  if (tid == 0) *n_tiles = min(tiles_total, max_tiles);
+  if (tid == 0) {
+    *n_tiles = min(tiles_total, max_tiles);
+    *n_groups = groups_total;
+  }
 
   // 4) per-chunk bases: walk chunks in order, one column per thread
   for (int c = tid; c < ES; c += kScanThreads) {
@@ -133,10 +142,9 @@ __global__ __launch_bounds__(kScanThreads) void perm_scan_kernel(
 
 // One block per chunk, one token per thread.  `elem_bytes` is 2 (bf16) or 4.
 __global__ __launch_bounds__(kPermChunk) void perm_scatter_kernel(
-    RunTable rt, int elem_bytes, const int32_t* __restrict__ chunk_base,
-    int32_t* __restrict__ perm, int32_t* __restrict__ inv, uint8_t* __restrict__ a_perm) {
+    RunTable rt, const int32_t* __restrict__ chunk_base, int32_t* __restrict__ perm,
+    int32_t* __restrict__ inv) {
   __shared__ unsigned long long mask[kPermChunk / kWave][1024];
-  __shared__ int pos_s[kPermChunk][kMaxSlots];
   const int E = rt.E, S = rt.S, k = rt.k, ES = E + S, slots = k + S;
   const int b = blockIdx.x;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -148,14 +156,9 @@ __global__ __launch_bounds__(kPermChunk) void perm_scatter_kernel(
   const int t0 = (b - rt.chunk_base[rho]) * kPermChunk;
   const int t = t0 + threadIdx.x;
   const bool valid = t < T;
-  int ex[kMaxSlots];
-  if (valid) {
-    const int32_t* ix = rt.idx[rho] + (size_t)t * k;
-    for (int r = 0; r < k; ++r) {
-      ex[r] = clamp_expert(ix[r], E);
-      atomicOr(&mask[wave][ex[r]], 1ull << lane);
-    }
-  }
+  const int32_t* ix = rt.idx[rho] + (size_t)t * k;
+  if (valid)
+    for (int r = 0; r < k; ++r) atomicOr(&mask[wave][clamp_expert(ix[r], E)], 1ull << lane);
   __syncthreads();
   if (valid) {
     const unsigned long long below = (1ull << lane) - 1ull;
@@ -164,33 +167,34 @@ __global__ __launch_bounds__(kPermChunk) void perm_scatter_kernel(
     for (int r = 0; r < slots; ++r) {
       int pos;
       if (r < k) {
-        const int e = ex[r];
+        const int e = clamp_expert(ix[r], E);
         int rank = __popcll(mask[wave][e] & below);
         for (int w2 = 0; w2 < wave; ++w2) rank += __popcll(mask[w2][e]);
         pos = cb[e] + rank;
       } else {
         pos = cb[E + (r - k)] + threadIdx.x;  // every token of the chunk has it
       }
-      pos_s[threadIdx.x][r] = pos;
       inv[q0 + r] = pos;
-      if (perm) perm[pos] = (int32_t)(q0 + r);
+      perm[pos] = (int32_t)(q0 + r);
     }
   }
-  __syncthreads();
-  // row copies: each wavefront moves its 64 tokens' rows, 16 bytes per lane
+}
+
+__global__ __launch_bounds__(256) void gather_rows_kernel(RunTable rt, int P, int elem_bytes,
+                                                          const int32_t* __restrict__ perm,
+                                                          uint8_t* __restrict__ a_perm) {
+  const int lane = threadIdx.x & 63;
+  const int p = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (p >= P) return;
+  const int slots = rt.k + rt.S;
+  const int g = min(max(perm[p], 0), P - 1) / slots;  // global token of the pair
+  const int rho = find_entry(rt.tok_base, rt.n, g);
+  const int t = g - rt.tok_base[rho];
   const size_t row_bytes = (size_t)rt.H * elem_bytes;
+  const uint4* src = reinterpret_cast<const uint4*>(static_cast<const uint8_t*>(rt.a[rho]) + (size_t)t * row_bytes);
+  uint4* dst = reinterpret_cast<uint4*>(a_perm + (size_t)p * row_bytes);
   const int n16 = (int)(row_bytes / 16);
-  const uint8_t* a_base = static_cast<const uint8_t*>(rt.a[rho]);
-  for (int i = 0; i < kWave; ++i) {
-    const int tl = wave * kWave + i;
-    if (t0 + tl >= T) break;
-    const uint4* src = reinterpret_cast<const uint4*>(a_base + (size_t)(t0 + tl) * row_bytes);
-    for (int c = lane; c < n16; c += kWave) {
-      const uint4 v = src[c];
-      for (int r = 0; r < slots; ++r)
-        reinterpret_cast<uint4*>(a_perm + (size_t)pos_s[tl][r] * row_bytes)[c] = v;
-    }
-  }
+  for (int c = lane; c < n16; c += 64) dst[c] = src[c];
 }
 
 }  // namespace
@@ -204,22 +208,27 @@ hipError_t launch_perm_count(const RunTable& rt, int n_chunks, int32_t* hist, hi
 
 hipError_t launch_perm_scan(const RunTable& rt, int n_chunks, const int32_t* hist,
                             int32_t* chunk_base, int32_t* offsets, int2* tiles,
-                            int32_t* n_tiles, int bm, int max_tiles, hipStream_t s) {
+                            int32_t* n_tiles, int4* groups, int32_t* n_groups, int bm,
+                            int max_tiles, hipStream_t s) {
   const size_t smem = sizeof(int) * ((size_t)rt.L * (rt.E + rt.S) + kScanThreads);
   prof_start(EB_K_PERM_SCAN, s);
   hipLaunchKernelGGL(perm_scan_kernel, dim3(1), dim3(kScanThreads), smem, s, rt, n_chunks, hist,
-                     chunk_base, offsets, tiles, n_tiles, bm, max_tiles);
+                     chunk_base, offsets, tiles, n_tiles, groups, n_groups, bm, max_tiles);
   prof_stop(EB_K_PERM_SCAN, s);
   return hipGetLastError();
 }
 
-hipError_t launch_perm_scatter(const RunTable& rt, int n_chunks, int elem_bytes,
+hipError_t launch_perm_scatter(const RunTable& rt, int n_chunks, int P, int elem_bytes,
                                const int32_t* chunk_base, int32_t* perm, int32_t* inv,
                                void* a_perm, hipStream_t s) {
   prof_start(EB_K_PERM_SCATTER, s);
-  hipLaunchKernelGGL(perm_scatter_kernel, dim3(n_chunks), dim3(kPermChunk), 0, s, rt, elem_bytes,
-                     chunk_base, perm, inv, static_cast<uint8_t*>(a_perm));
+  hipLaunchKernelGGL(perm_scatter_kernel, dim3(n_chunks), dim3(kPermChunk), 0, s, rt, chunk_base,
+                     perm, inv);
   prof_stop(EB_K_PERM_SCATTER, s);
+  prof_start(EB_K_PERM_GATHER, s);
+  hipLaunchKernelGGL(gather_rows_kernel, dim3((P + 3) / 4), dim3(256), 0, s, rt, P, elem_bytes, perm,
+                     static_cast<uint8_t*>(a_perm));
+  prof_stop(EB_K_PERM_GATHER, s);
   return hipGetLastError();
 }
 

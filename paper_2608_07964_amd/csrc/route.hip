@@ -1,7 +1,10 @@
 // Routing of one micro-batch at one layer (Section 2.1: W, I = topk(G(h'))):
-//   rmsnorm_kernel  a = dtype(x * r * gain), one wavefront per token
-//   logits_kernel   z = a Wg^T + bias, LDS-tiled fp32 VALU GEMM (E is small)
-//   topk_kernel     top-k by wavefront argmax, softmax weights, expert counts
+//   norm_router_kernel  E <= 64: one wavefront per token computes
+//                       a = dtype(x * r * gain) and z = a Wg^T + bias in one pass
+//                       (Wg stays in L2; lane partial sums, butterfly reductions)
+//   rmsnorm_kernel +    E > 64: RMSNorm, then an LDS-tiled fp32 VALU GEMM for z
+//   logits_kernel
+//   topk_kernel         top-k by wavefront argmax, softmax weights, expert counts
 #include <math.h>
 
 #include "eb_internal.h"
@@ -97,6 +100,70 @@ __global__ __launch_bounds__(256) void logits_kernel(int T, int H, int E, const 
     for (int j = 0; j < 4; ++j) {
       const int e = e0 + tx + 16 * j;
       if (e < E) z[(size_t)t * E + e] = acc[i][j] + bias[e];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Fused RMSNorm + router logits for E <= EMAX.  Lane l owns the 8-element
+// chunks starting at h = 8 (l + 64 i); per chunk it forms the stored a values and adds
+// their products with every router row into one accumulator per expert; each
+// expert's lane partial sums are then reduced by a butterfly (bit-identical
+// total in every lane) and lane e writes z[t][e].
+template <typename TA, int EMAX>
+__global__ __launch_bounds__(256) void norm_router_kernel(int T, int H, int E, const float* __restrict__ x,
+                                                          const float* __restrict__ gain,
+                                                          const TA* __restrict__ Wg,
+                                                          const float* __restrict__ bias,
+                                                          TA* __restrict__ a, float* __restrict__ z,
+                                                          float eps) {
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;
+  const float* xr = x + (size_t)t * H;
+  const int nchunk = H >> 3;  // 8-element chunks; lane l takes chunks l, l + 64, ...
+  float ss = 0.f;
+  for (int c = lane; c < nchunk; c += 64) {
+    const float4* p4 = reinterpret_cast<const float4*>(xr + 8 * c);
+    const float4 u = p4[0], v = p4[1];
+    ss = fmaf(u.x, u.x, ss); ss = fmaf(u.y, u.y, ss); ss = fmaf(u.z, u.z, ss); ss = fmaf(u.w, u.w, ss);
+    ss = fmaf(v.x, v.x, ss); ss = fmaf(v.y, v.y, ss); ss = fmaf(v.z, v.z, ss); ss = fmaf(v.w, v.w, ss);
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off, 64);
+  const float r = 1.0f / sqrtf(ss / (float)H + eps);
+  float acc[EMAX];
+#pragma unroll
+  for (int e = 0; e < EMAX; ++e) acc[e] = 0.f;
+  TA* ar = a + (size_t)t * H;
+  for (int c = lane; c < nchunk; c += 64) {
+    const int h = 8 * c;
+    const float4* p4 = reinterpret_cast<const float4*>(xr + h);
+    const float4* g4 = reinterpret_cast<const float4*>(gain + h);
+    const float4 u = p4[0], v = p4[1], gu = g4[0], gv = g4[1];
+    float av[8] = {u.x * r * gu.x, u.y * r * gu.y, u.z * r * gu.z, u.w * r * gu.w,
+                   v.x * r * gv.x, v.y * r * gv.y, v.z * r * gv.z, v.w * r * gv.w};
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      Elem<TA>::store(ar, h + q, av[q]);
+      av[q] = Elem<TA>::round(av[q]);  // the stored (rounded) value feeds the router
+    }
+#pragma unroll
+    for (int e = 0; e < EMAX; ++e) {
+      if (e < E) {
+        const TA* wr = Wg + (size_t)e * H + h;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) acc[e] = fmaf(av[q], Elem<TA>::load(wr, q), acc[e]);
+      }
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < EMAX; ++e) {
+    if (e < E) {
+      float v = acc[e];
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+      if (lane == e) z[(size_t)t * E + e] = v + bias[e];
     }
   }
 }
@@ -199,15 +266,28 @@ hipError_t route_typed(const eb_model_desc& d, int T, const float* x, const floa
                        int32_t* idx, float* w, int32_t* counts, hipStream_t s) {
   hipLaunchKernelGGL(zero_i32_kernel, dim3((d.E + 255) / 256), dim3(256), 0, s, counts, d.E);
   if (T == 0) return hipGetLastError();
-  prof_start(EB_K_ROUTE_NORM, s);
-  hipLaunchKernelGGL(rmsnorm_kernel<TA>, dim3((T + 3) / 4), dim3(256), 0, s, T, d.H, x, gain,
-                     static_cast<TA*>(a_out), d.rms_eps);
-  prof_stop(EB_K_ROUTE_NORM, s);
-  prof_start(EB_K_ROUTE_LOGITS, s);
-  hipLaunchKernelGGL(logits_kernel<TA>, dim3((T + LG_BT - 1) / LG_BT, (d.E + LG_BE - 1) / LG_BE),
-                     dim3(256), 0, s, T, d.H, d.E, static_cast<const TA*>(a_out),
-                     static_cast<const TA*>(Wg), bias, logits);
-  prof_stop(EB_K_ROUTE_LOGITS, s);
+  if (d.E <= 64) {
+    prof_start(EB_K_ROUTE_LOGITS, s);
+    if (d.E <= 8)
+      hipLaunchKernelGGL((norm_router_kernel<TA, 8>), dim3((T + 3) / 4), dim3(256), 0, s, T, d.H, d.E,
+                         x, gain, static_cast<const TA*>(Wg), bias, static_cast<TA*>(a_out), logits,
+                         d.rms_eps);
+    else
+      hipLaunchKernelGGL((norm_router_kernel<TA, 64>), dim3((T + 3) / 4), dim3(256), 0, s, T, d.H,
+                         d.E, x, gain, static_cast<const TA*>(Wg), bias, static_cast<TA*>(a_out),
+                         logits, d.rms_eps);
+    prof_stop(EB_K_ROUTE_LOGITS, s);
+  } else {
+    prof_start(EB_K_ROUTE_NORM, s);
+    hipLaunchKernelGGL(rmsnorm_kernel<TA>, dim3((T + 3) / 4), dim3(256), 0, s, T, d.H, x, gain,
+                       static_cast<TA*>(a_out), d.rms_eps);
+    prof_stop(EB_K_ROUTE_NORM, s);
+    prof_start(EB_K_ROUTE_LOGITS, s);
+    hipLaunchKernelGGL(logits_kernel<TA>, dim3((T + LG_BT - 1) / LG_BT, (d.E + LG_BE - 1) / LG_BE),
+                       dim3(256), 0, s, T, d.H, d.E, static_cast<const TA*>(a_out),
+                       static_cast<const TA*>(Wg), bias, logits);
+    prof_stop(EB_K_ROUTE_LOGITS, s);
+  }
   prof_start(EB_K_ROUTE_TOPK, s);
   hipLaunchKernelGGL(topk_kernel, dim3((T + 3) / 4), dim3(256), 0, s, T, d.E, d.k, d.norm_topk,
                      logits, idx, w, counts);

@@ -26,7 +26,9 @@ This module holds no arithmetic of the method itself.
 """
 from __future__ import annotations
 
+import ctypes
 import functools
+import os
 import statistics
 
 import numpy as np
@@ -86,9 +88,40 @@ def _mix64_np(z: np.ndarray) -> np.ndarray:
     return z
 
 
+_HOST_LIB = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsynthhost.so")
+_host = None
+
+
+def _host_lib():
+    """The C/OpenMP implementation of the same stream (gen_host.c), if built."""
+    global _host
+    if _host is None and os.path.exists(_HOST_LIB):
+        l = ctypes.CDLL(_HOST_LIB)
+        l.synth_host_normal.restype = None
+        l.synth_host_normal.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int64,
+                                        ctypes.c_void_p, ctypes.c_float, ctypes.c_int,
+                                        ctypes.c_void_p]
+        _host = l
+    return _host
+
+
+def normal_values(key: int, i0: int, n: int, sigma: np.float32, as_bf16: bool) -> np.ndarray:
+    """Elements i0 .. i0+n-1 of stream ``key`` as fp32 (rounded to bf16 values
+    if ``as_bf16``); uses the compiled generator when it is built."""
+    l = _host_lib()
+    if l is None:
+        v = normal_f32(key, i0, n, sigma)
+        return bf16_bits_to_f32(f32_to_bf16_bits(v)) if as_bf16 else v
+    out = np.empty(n, dtype=np.float32)
+    tab = normal_table()
+    l.synth_host_normal(key, i0, n, tab.ctypes.data, float(sigma), int(as_bf16), out.ctypes.data)
+    return out
+
+
 def normal_f32(key: int, i0: int, n: int, sigma: np.float32,
                chunk: int = 1 << 23) -> np.ndarray:
-    """fp32 values of elements i0 .. i0+n-1 of the stream ``key``."""
+    """fp32 values of elements i0 .. i0+n-1 of the stream ``key`` (NumPy
+    reference implementation of the definition above)."""
     tab = normal_table()
     out = np.empty(n, dtype=np.float32)
     k = np.uint64(key)
@@ -116,10 +149,8 @@ def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
 def tensor_values(cfg: Config, kind: int, index: int, i0: int, n: int) -> np.ndarray:
     """Elements [i0, i0+n) of a generated tensor as the stored values, in fp32
     (for bf16 storage: the fp32 value of the stored bf16).  x is always fp32."""
-    v = normal_f32(stream_key(cfg.seed, kind, index), i0, n, sigma_of(kind, cfg.H))
-    if cfg.dtype == "bf16" and kind != KIND_X:
-        v = bf16_bits_to_f32(f32_to_bf16_bits(v))
-    return v
+    return normal_values(stream_key(cfg.seed, kind, index), i0, n, sigma_of(kind, cfg.H),
+                         cfg.dtype == "bf16" and kind != KIND_X)
 
 
 # ---- whole tensors / slices used by tests and the oracle -------------------

@@ -71,3 +71,14 @@ def test_config_shapes():
     for cfg in CONFIGS:
         assert cfg.E % cfg.D == 0 and cfg.H % 256 == 0 and cfg.F % 128 == 0
     assert [c.m for c in CONFIGS] == [1, 3, 6, 12, 6]
+
+
+def test_compiled_host_generator_matches_numpy_definition():
+    assert gen._host_lib() is not None, "synth/libsynthhost.so is not built"
+    for kind, dt in [(gen.KIND_X, False), (gen.KIND_GU, True), (gen.KIND_WG, True)]:
+        key = gen.stream_key(20260003, kind, 5)
+        sig = gen.sigma_of(kind, 2048)
+        ref = gen.normal_f32(key, 123456789, 300001, sig)
+        if dt:
+            ref = gen.bf16_bits_to_f32(gen.f32_to_bf16_bits(ref))
+        assert np.array_equal(gen.normal_values(key, 123456789, 300001, sig, dt), ref)
