@@ -28,7 +28,7 @@
  *    accumulation is always fp32.
  *  - Shape limits (EB_ERR_UNSUPPORTED otherwise): H % 256 == 0,
  *    F % 128 == 0, 1 <= k <= E, E + S <= 1024, k + S <= 16, E % D == 0,
- *    L <= EB_MAX_LAYERS, L * (E + S) <= 15360.
+ *    L <= EB_MAX_LAYERS, L * (E + S) <= 15360; bf16 stacks: E <= 256.
  */
 #ifndef EASYBALANCE_H
 #define EASYBALANCE_H

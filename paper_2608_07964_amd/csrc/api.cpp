@@ -34,6 +34,8 @@ int check_desc(const eb_model_desc* d) {
   if (d->H % 256 != 0) return set_error(EB_ERR_UNSUPPORTED, "H=%d is not a multiple of 256", d->H);
   if (d->F % 128 != 0) return set_error(EB_ERR_UNSUPPORTED, "F=%d is not a multiple of 128", d->F);
   if (d->E + d->S > 1024) return set_error(EB_ERR_UNSUPPORTED, "E+S=%d > 1024", d->E + d->S);
+  if (d->dtype == EB_DTYPE_BF16 && d->E > 256)
+    return set_error(EB_ERR_UNSUPPORTED, "bf16 router supports E <= 256 (E=%d)", d->E);
   if (d->k + d->S > kMaxSlots) return set_error(EB_ERR_UNSUPPORTED, "k+S=%d > %d", d->k + d->S, kMaxSlots);
   if (d->L > EB_MAX_LAYERS) return set_error(EB_ERR_UNSUPPORTED, "L=%d > %d", d->L, EB_MAX_LAYERS);
   if ((long)d->L * (d->E + d->S) > 15360)

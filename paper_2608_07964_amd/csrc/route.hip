@@ -1,9 +1,11 @@
 // Routing of one micro-batch at one layer (Section 2.1: W, I = topk(G(h'))):
-//   norm_router_kernel  E <= 64: one wavefront per token computes
+//   norm_router_kernel  E <= 8 (bf16) / E <= 64 (fp32): one wavefront per token computes
 //                       a = dtype(x * r * gain) and z = a Wg^T + bias in one pass
 //                       (Wg stays in L2; lane partial sums, butterfly reductions)
-//   rmsnorm_kernel +    E > 64: RMSNorm, then an LDS-tiled fp32 VALU GEMM for z
-//   logits_kernel
+//   rmsnorm_kernel +    bf16 stacks with E > 8: RMSNorm, then the router GEMM on
+//   router_mfma_kernel  the matrix cores (split-K over the 4 wavefronts)
+//   rmsnorm_kernel +    fp32 stacks with E > 64: RMSNorm, then an LDS-tiled fp32
+//   logits_kernel       VALU GEMM for z
 //   topk_kernel         top-k by wavefront argmax, softmax weights, expert counts
 #include <math.h>
 
@@ -169,6 +171,88 @@ __global__ __launch_bounds__(256) void norm_router_kernel(int T, int H, int E, c
 }
 
 // ---------------------------------------------------------------------------
+// Router logits on the matrix cores (bf16 stacks, 8 < E <= 256):
+// z[T][E] = a Wg^T + bias.  A workgroup takes 32 tokens and all experts
+// (padded to NB blocks of 32); its 4 wavefronts split K into quarters, each
+// accumulating a 32 x 32 NB partial with v_mfma_f32_32x32x16_bf16 from
+// operands loaded straight from L2 into registers (one 32-wide K chunk
+// prefetched).  Waves 1..3 leave their partials in LDS and wave 0 adds them in
+// that order, then adds the bias: a fixed summation order, so the logits of a
+// micro-batch do not depend on anything but its inputs.
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float floatx16_t __attribute__((ext_vector_type(16)));
+
+template <int NB>
+__global__ __launch_bounds__(256) void router_mfma_kernel(int T, int H, int E,
+                                                          const bf16_t* __restrict__ a,
+                                                          const bf16_t* __restrict__ Wg,
+                                                          const float* __restrict__ bias,
+                                                          float* __restrict__ z) {
+  __shared__ float part[3][NB][16][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lrow = lane & 31, khalf = lane >> 5;
+  const int t0 = blockIdx.x * 32;
+  const int kq = H / 4, kbeg = wave * kq;
+  // this lane's A row (token) and B rows (experts), clamped into range
+  const bf16_t* arow = a + (size_t)min(t0 + lrow, T - 1) * H + kbeg + 8 * khalf;
+  const bf16_t* brow[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+    brow[nb] = Wg + (size_t)min(nb * 32 + lrow, E - 1) * H + kbeg + 8 * khalf;
+  floatx16_t acc[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[nb][v] = 0.f;
+  // a 32-wide K chunk = two MFMA k-steps of 16
+  bf16x8_t ac[2][2], bc[2][NB][2];
+  auto load = [&](int buf, int k) {
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      ac[buf][s] = *reinterpret_cast<const bf16x8_t*>(arow + k + 16 * s);
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+        bc[buf][nb][s] = *reinterpret_cast<const bf16x8_t*>(brow[nb] + k + 16 * s);
+    }
+  };
+  auto mma = [&](int buf) {
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+        acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ac[buf][s], bc[buf][nb][s], acc[nb], 0, 0, 0);
+  };
+  load(0, 0);
+  for (int k = 0; k < kq; k += 64) {
+    if (k + 32 < kq) load(1, k + 32);
+    mma(0);
+    if (k + 64 < kq) load(0, k + 64);
+    if (k + 32 < kq) mma(1);
+  }
+  if (wave > 0) {
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) part[wave - 1][nb][v][lane] = acc[nb][v];
+  }
+  __syncthreads();
+  if (wave != 0) return;
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      float sum = acc[nb][v];
+#pragma unroll
+      for (int w = 0; w < 3; ++w) sum += part[w][nb][v][lane];
+      // C[row][col]: col = lane % 32 of block nb (expert), row = 8 (v/4) + 4 (lane/32) + v%4 (token)
+      const int t = t0 + 8 * (v >> 2) + 4 * khalf + (v & 3);
+      const int e = nb * 32 + lrow;
+      if (t < T && e < E) z[(size_t)t * E + e] = sum + bias[e];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Top-k, softmax weights and expert counts.  One wavefront per token; lane l
 // holds logits e = l + 64 s.  Each pick is a wavefront argmax under the total
 // order (larger z first, then lower expert id), so every lane agrees.
@@ -266,7 +350,25 @@ hipError_t route_typed(const eb_model_desc& d, int T, const float* x, const floa
                        int32_t* idx, float* w, int32_t* counts, hipStream_t s) {
   hipLaunchKernelGGL(zero_i32_kernel, dim3((d.E + 255) / 256), dim3(256), 0, s, counts, d.E);
   if (T == 0) return hipGetLastError();
-  if (d.E <= 64) {
+  if (sizeof(TA) == 2 && d.E > 8) {
+    // RMSNorm, then the router GEMM on the matrix cores
+    prof_start(EB_K_ROUTE_NORM, s);
+    hipLaunchKernelGGL(rmsnorm_kernel<TA>, dim3((T + 3) / 4), dim3(256), 0, s, T, d.H, x, gain,
+                       static_cast<TA*>(a_out), d.rms_eps);
+    prof_stop(EB_K_ROUTE_NORM, s);
+    prof_start(EB_K_ROUTE_LOGITS, s);
+    const dim3 grid((T + 31) / 32);
+    const bf16_t* ab = static_cast<const bf16_t*>(a_out);
+    const bf16_t* wb = static_cast<const bf16_t*>(Wg);
+    const int nb = (d.E + 31) / 32;
+    if (nb <= 2)
+      hipLaunchKernelGGL(router_mfma_kernel<2>, grid, dim3(256), 0, s, T, d.H, d.E, ab, wb, bias, logits);
+    else if (nb <= 4)
+      hipLaunchKernelGGL(router_mfma_kernel<4>, grid, dim3(256), 0, s, T, d.H, d.E, ab, wb, bias, logits);
+    else
+      hipLaunchKernelGGL(router_mfma_kernel<8>, grid, dim3(256), 0, s, T, d.H, d.E, ab, wb, bias, logits);
+    prof_stop(EB_K_ROUTE_LOGITS, s);
+  } else if (d.E <= 64) {
     prof_start(EB_K_ROUTE_LOGITS, s);
     if (d.E <= 8)
       hipLaunchKernelGGL((norm_router_kernel<TA, 8>), dim3((T + 3) / 4), dim3(256), 0, s, T, d.H, d.E,
