@@ -162,6 +162,15 @@ __device__ __forceinline__ void k_loop(const KLoop& L, floatx16 (&acc)[4][4]) {
       if (NACT > 0) {
         read_frags<NACT>(L, kt, ks + 1, f[(ks + 1) & 1]);
         mfmas<NACT>(f[ks & 1], acc);
+        // keep the next k-step's fragment reads spread between this k-step's
+        // MFMAs (the machine scheduler would otherwise move reads next to
+        // their consumers and expose LDS latency)
+#pragma unroll
+        for (int i = 0; i < NACT + 4; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one DS read
+          __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // two MFMAs
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, 4 * NACT - 2 * (NACT + 4) > 0 ? 4 * NACT - 2 * (NACT + 4) : 0, 0);
       }
     }
     // every fragment of stage kt is in registers, stage kt+1 has landed
