@@ -32,23 +32,52 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 enum { MODE_GATEUP = 0, MODE_DOWN = 1 };
 
-// bf16 tiles: 256 x 256 output per workgroup of 4 wavefronts (one per SIMD),
-// each owning a 128 x 128 quarter as 4 x 4 MFMA 32x32 blocks (accumulators in
-// AGPRs): 8 fragment reads per 16 MFMAs.  K advances 64 at a time, so every
-// 128-byte line of A and B is consumed whole by one stage; two LDS stages of
-// 64 KB (A and B tiles of 256 rows x 128 bytes) are filled by buffer loads
-// straight into LDS one stage ahead.  Fragments of the next k-step are read
-// while the MFMAs of the current one run, and the per-stage barrier sits
-// before the last k-step's MFMAs, so neither the barrier nor LDS latency
-// stalls the matrix cores.
-constexpr int BM = 256, BN = 256, BK = 64;
-constexpr int kStages = 2;
-constexpr int kThreads = 256;
+// bf16 tiles.  Every tile is BM x 256 outputs on a workgroup of 4 wavefronts
+// (one per SIMD) and K advances 64 at a time, so every 128-byte line of A and
+// B is consumed whole by one stage; stages are filled by buffer loads straight
+// into LDS.  The B tile (256 weight rows x 64 k) is the same in every shape;
+// the shape of an m-tile follows the rows it holds:
+//
+//   BM 256 (> 128 rows): 2 x 4 wavefronts of 128 x 64 (4 x 2 MFMA blocks),
+//          A ring of 2 stages (32 KB each), B ring of 3 stages (32 KB each);
+//   BM 128 (65..128 rows): 2 x 4 wavefronts of 64 x 64, 3 stages of A and B;
+//   BM 64  (<= 64 rows): 2 x 4 wavefronts of 32 x 64, 4 stages of A and B.
+//
+// Eight wavefronts (two per SIMD) keep each matrix core fed while the other
+// wavefront of its SIMD waits on a barrier or on LDS.  Groups that run few
+// m-tiles are bound by streaming their expert's weights from HBM, which needs
+// many bytes in flight per CU: every shape keeps at least two B stages in
+// flight.  Fragments of the next k-step are read while the MFMAs of the
+// current one run, and the per-stage barrier sits before the last k-step's
+// MFMAs.
+constexpr int BN = 256, BK = 64;
+constexpr int kWaves = 8;                        // two wavefronts per SIMD
+constexpr int kThreads = 64 * kWaves;
 constexpr int kKsteps = BK / 16;                 // MFMA k-steps per stage
-constexpr int kTileElems = BM * BK;              // one operand tile of a stage
-constexpr int kStageElems = 2 * kTileElems;      // A then B
-constexpr int kRowBlocks = 8;                    // 8-row blocks per wave per operand
+constexpr int kBLoads = BN / (8 * kWaves);       // 8-row B blocks per wave per stage
 constexpr int kXcds = 8;
+
+template <int BM_, int WM_, int SA_, int SB_>
+struct TileCfg {
+  static constexpr int BM = BM_;                 // tile rows
+  static constexpr int WM = WM_, WN = kWaves / WM_;  // wavefront grid
+  static constexpr int SA = SA_, SB = SB_;       // LDS stages of the A and B rings
+  static constexpr int TM = BM / WM, TN = BN / WN;  // wavefront tile
+  static constexpr int MB = TM / 32, NB = TN / 32;  // MFMA blocks per wavefront
+  static constexpr int A_LOADS = BM / (8 * kWaves);  // 8-row A blocks per wave per stage
+  static constexpr int A_ELEMS = BM * BK, B_ELEMS = BN * BK;  // one stage of each ring
+  static constexpr int B_RING = SA * A_ELEMS;    // LDS element offset of the B ring
+  static constexpr int LDS_ELEMS = SA * A_ELEMS + SB * B_ELEMS;
+  static_assert(MB >= 1 && NB >= 2 && A_LOADS >= 1, "tile shape");
+  static_assert(SA >= 2 && (SB == SA || SB == SA + 1), "ring depths");
+};
+using CfgBig = TileCfg<256, 2, 2, 3>;
+using CfgMid = TileCfg<128, 2, 3, 3>;
+using CfgSkinny = TileCfg<64, 2, 4, 4>;
+constexpr int cmax(int a, int b) { return a > b ? a : b; }
+constexpr int kLdsElems = cmax(cmax(CfgBig::LDS_ELEMS, CfgMid::LDS_ELEMS), CfgSkinny::LDS_ELEMS);
+static_assert(kLdsElems * 2 <= 160 * 1024, "LDS budget");
+constexpr int BM = CfgBig::BM;                   // row-block granularity of the tile list
 
 // 128-byte LDS rows hold eight 16-byte chunks; logical chunk c of row r sits
 // at c ^ ((r >> 1) & 7).  A ds_read_b128 phase of 16 lanes reads 16
@@ -60,9 +89,26 @@ __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >>
 // s_waitcnt immediates (gfx9 encoding: vmcnt bits 3:0 and 15:14, expcnt
 // 6:4, lgkmcnt 11:8).  Issued through the builtin so that the compiler's own
 // wait insertion sees them and does not add conservative waits of its own.
-constexpr int kWaitVm0 = (7 << 4) | (15 << 8);
-constexpr int kWaitVm16 = (16 >> 4) << 14 | (7 << 4) | (15 << 8);
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
 constexpr int kWaitLgkm0 = 15 | (3 << 14) | (7 << 4);
+
+// Wait until at most n of this wave's loads are in flight: the largest rung
+// <= n of a ladder that holds every count the K loops below ask for.
+__device__ __forceinline__ void wait_le(int n) {
+  if (n >= 16) wait_vm<16>();
+  else if (n >= 15) wait_vm<15>();
+  else if (n >= 12) wait_vm<12>();
+  else if (n >= 10) wait_vm<10>();
+  else if (n >= 8) wait_vm<8>();
+  else if (n >= 6) wait_vm<6>();
+  else if (n >= 5) wait_vm<5>();
+  else if (n >= 4) wait_vm<4>();
+  else wait_vm<0>();
+}
 
 // Bare workgroup barrier: this wave's outstanding buffer->LDS loads stay in
 // flight across it (a fenced __syncthreads would drain them).
@@ -77,141 +123,306 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, 
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
 
-// Load slots: wave w fills LDS rows 64 w + 8 j .. +7 of each operand tile
-// (j < 8); lane l supplies row r_j = 64 w + 8 j + l / 8 at physical chunk
-// l % 8, i.e. logical chunk c_j = (l % 8) ^ ((r_j >> 1) & 7), which is c_0 for
-// even j and c_0 ^ 4 for odd j.  A row r_j and B row brow0 + 8 j (see the item
-// setup) are affine in j, so a load's byte offset is a per-lane part that
-// depends only on the parity of j plus a wave-uniform part (soffset).  A rows
-// past the group's end lie outside the A descriptor's range and read zeros.
+// Load slots: in every stage wave w fills A rows (BM/4) w + 8 j + l/8
+// (j < BM/32) and B rows 64 w + 8 j + l/8 (j < 8) of the tile, lane l at
+// physical chunk l % 8, i.e. logical chunk (l % 8) ^ ((r >> 1) & 7), which is
+// c0 for even j and c0 ^ 4 for odd j (every block base is a multiple of 16
+// rows).  A load's byte offset is a per-lane part (row l/8 of the block and
+// the chunk, by parity of j) plus a wave-uniform part (the block's first
+// global row and the stage's K offset) passed as soffset.  A rows past the
+// buffer's end read zeros; rows past the group's end are loaded but their
+// results are discarded.
 struct KLoop {
   bf16_t* smem;
   __amdgpu_buffer_rsrc_t ra, rb;   // buffer descriptors of the A tile and the expert's B
   int a_lane[2], b_lane[2];        // per-lane byte offsets for even / odd j
+  int a_row0;                      // first A row (within the tile) of the wave's load blocks
+  int b_row[kBLoads];              // first global B row of each of the wave's load blocks
   int row_bytes;                   // K * 2
-  int lds_load;                    // LDS element offset of the wave's first load row
+  int lds_a_load, lds_b_load;      // LDS element offsets of the wave's first A / B load rows
   int lds_a, lds_b;                // LDS element offsets of this lane's fragment rows (chunk-free)
   int sw;                          // this lane's fragment swizzle ((row >> 1) & 7)
   int nk, khalf;
 };
 
+template <class C>
 struct Frags {
-  bf16x8 a[4], b[4];
+  bf16x8 a[C::MB], b[C::NB];
 };
 
-// Fragment rows of one lane: A rows wm*128 + mb*32 + lrow, B rows
-// wn*128 + nb*32 + lrow; (row >> 1) & 7 = (lrow >> 1) & 7 for all of them, so
-// one chunk term per k-step serves every block and the block offsets are
-// immediates.
-template <int NACT>
-__device__ __forceinline__ void read_frags(const KLoop& L, int stage, int ks, Frags& f) {
-  const bf16_t* base = L.smem + (stage % kStages) * kStageElems + ((ks * 2 + L.khalf) ^ L.sw) * 8;
+// Loads of stage s (K columns 64 s .. 64 s + 63) of A into A slot sa and of
+// B into B slot sb.
+template <class C>
+__device__ __forceinline__ void issue_a(const KLoop& L, int s, int slot) {
+  bf16_t* d = L.smem + slot * C::A_ELEMS + L.lds_a_load;
+  const int ko = s * BK * 2;
 #pragma unroll
-  for (int mb = 0; mb < NACT; ++mb)
-    f.a[mb] = *reinterpret_cast<const bf16x8*>(base + L.lds_a + mb * 32 * BK);
+  for (int j = 0; j < C::A_LOADS; ++j)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(L.ra, d + j * 8 * BK, 16, L.a_lane[j & 1],
+                                             (L.a_row0 + 8 * j) * L.row_bytes + ko, 0, 0);
+}
+template <class C>
+__device__ __forceinline__ void issue_b(const KLoop& L, int s, int slot) {
+  bf16_t* d = L.smem + C::B_RING + slot * C::B_ELEMS + L.lds_b_load;
+  const int ko = s * BK * 2;
 #pragma unroll
-  for (int nb = 0; nb < 4; ++nb)
-    f.b[nb] = *reinterpret_cast<const bf16x8*>(base + kTileElems + L.lds_b + nb * 32 * BK);
+  for (int j = 0; j < kBLoads; ++j)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(L.rb, d + j * 8 * BK, 16, L.b_lane[j & 1],
+                                             L.b_row[j] * L.row_bytes + ko, 0, 0);
 }
 
-template <int NACT>
-__device__ __forceinline__ void mfmas(const Frags& f, floatx16 (&acc)[4][4]) {
+// Load order: the prologue issues A(s) (s < SA) and B(s) (s < SB) for
+// s = 0, 1, ..., A before B; step kt issues A(kt+SA) then B(kt+SB) (stages
+// < nk only).  Loads complete in issue order, so "A(t) and B(t) have landed"
+// is "at most n loads are in flight", n = the loads issued after the later of
+// the two.
+template <class C>
+__device__ __forceinline__ int loads_after_stage0(int nk) {
+  int n = 0;
+#pragma unroll
+  for (int s = 1; s < C::SB; ++s) {
+    if (s < C::SA && s < nk) n += C::A_LOADS;
+    if (s < nk) n += kBLoads;
+  }
+  return n;
+}
+// In step kt, waiting for stage kt+1 (issued loads: prologue and steps < kt).
+template <class C>
+__device__ __forceinline__ int loads_after_next(int kt, int nk) {
+  int n = 0;
+  if (C::SB == C::SA) {
+    // A(t), B(t) are adjacent; after them come stages t+1 .. kt+SA-1
+#pragma unroll
+    for (int s = 2; s < C::SA; ++s)
+      if (kt + s < nk) n += C::A_LOADS + kBLoads;
+  } else {
+    // A(kt+1) is issued after B(kt+1); after it come B(kt+2), then the pairs
+    // A(kt+2..kt+SA-1), B(kt+3..kt+SA)
+    if (kt + 2 < nk) n += kBLoads;
+#pragma unroll
+    for (int s = 2; s < C::SA; ++s) {
+      if (kt + s < nk) n += C::A_LOADS;
+      if (kt + s + 1 < nk) n += kBLoads;
+    }
+  }
+  return n;
+}
+
+// Fragment rows of one lane: A rows wm*TM + mb*32 + lrow, B rows
+// wn*TN + nb*32 + lrow; (row >> 1) & 7 = (lrow >> 1) & 7 for all of them, so
+// one chunk term per k-step serves every block and the block offsets are
+// immediates.
+template <class C, int NACT>
+__device__ __forceinline__ void read_frags(const KLoop& L, int slot_a, int slot_b, int ks, Frags<C>& f) {
+  const int chunk = ((ks * 2 + L.khalf) ^ L.sw) * 8;
+  const bf16_t* ba = L.smem + slot_a * C::A_ELEMS + chunk;
+  const bf16_t* bb = L.smem + C::B_RING + slot_b * C::B_ELEMS + chunk;
+#pragma unroll
+  for (int mb = 0; mb < NACT; ++mb)
+    f.a[mb] = *reinterpret_cast<const bf16x8*>(ba + L.lds_a + mb * 32 * BK);
+#pragma unroll
+  for (int nb = 0; nb < C::NB; ++nb)
+    f.b[nb] = *reinterpret_cast<const bf16x8*>(bb + L.lds_b + nb * 32 * BK);
+}
+
+template <class C, int NACT>
+__device__ __forceinline__ void mfmas(const Frags<C>& f, floatx16 (&acc)[C::MB][C::NB]) {
 #pragma unroll
   for (int mb = 0; mb < NACT; ++mb)
 #pragma unroll
-    for (int nb = 0; nb < 4; ++nb)
+    for (int nb = 0; nb < C::NB; ++nb)
       acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[mb], f.b[nb], acc[mb][nb], 0, 0, 0);
 }
 
-// One item's K loop.  Stage s (K columns 64 s .. 64 s + 63) lives in LDS slot
-// s % 2.  In step kt the four k-steps of stage kt run with the next k-step's
-// fragments read ahead; before the MFMAs of the last k-step the wave waits for
-// its loads of stage kt+1 and its reads of stage kt, the barrier publishes
-// stage kt+1 and frees slot kt % 2, stage kt+2 is issued into it and the
-// first fragments of stage kt+1 are read.  NACT = active 32-row blocks of the
-// wave's 128 rows (inactive blocks of a ragged tile get neither LDS reads nor
-// MFMAs).
-template <int NACT>
-__device__ __forceinline__ void k_loop(const KLoop& L, floatx16 (&acc)[4][4]) {
-  // buffer (MUBUF) loads straight into LDS: lane l's 16 bytes land at the
-  // wave-uniform LDS address + 16 l
-  auto issue = [&](int s) {
-    bf16_t* sa = L.smem + (s % kStages) * kStageElems + L.lds_load;
-    bf16_t* sb = sa + kTileElems;
-#pragma unroll
-    for (int j = 0; j < kRowBlocks; ++j) {
-      const int so = j * 8 * L.row_bytes + s * BK * 2;  // wave-uniform
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(L.ra, sa + j * 8 * BK, 16, L.a_lane[j & 1], so, 0, 0);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(L.rb, sb + j * 8 * BK, 16, L.b_lane[j & 1], so, 0, 0);
-    }
-  };
-  const int nk = L.nk;
-  issue(0);
-  if (nk > 1) {
-    issue(1);
-    __builtin_amdgcn_s_waitcnt(kWaitVm16);
-  } else {
-    __builtin_amdgcn_s_waitcnt(kWaitVm0);
+// Scheduling groups that spread R fragment reads evenly between M MFMAs.
+template <int R, int M, int I = 0>
+__device__ __forceinline__ void interleave() {
+  if constexpr (I < R) {
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one DS read
+    constexpr int q = ((I + 1) * M) / R - (I * M) / R;
+    if constexpr (q > 0) __builtin_amdgcn_sched_group_barrier(0x008, q, 0);  // q MFMAs
+    interleave<R, M, I + 1>();
   }
+}
+
+// One item's K loop.  Stage s (K columns 64 s .. 64 s + 63) lives in A slot
+// s % SA and B slot s % SB.  In step kt the four k-steps of stage kt run with
+// the next k-step's fragments read ahead; before the MFMAs of the last k-step
+// the wave waits for its reads of stage kt and its loads of stage kt+1, the
+// barrier publishes stage kt+1 and frees the slots of stage kt, A(kt+SA) and
+// B(kt+SB) are issued into them and the first fragments of stage kt+1 are
+// read.  NACT = active 32-row blocks of the wave's rows (inactive blocks of a
+// ragged tile get neither LDS reads nor MFMAs).
+template <class C, int NACT>
+__device__ __forceinline__ void k_loop(const KLoop& L, floatx16 (&acc)[C::MB][C::NB]) {
+  const int nk = L.nk;
+#pragma unroll
+  for (int s = 0; s < C::SB; ++s) {
+    if (s < C::SA && s < nk) issue_a<C>(L, s, s);
+    if (s < nk) issue_b<C>(L, s, s);
+  }
+  wait_le(loads_after_stage0<C>(nk));
   bar();
-  Frags f[2];
-  if (NACT > 0) read_frags<NACT>(L, 0, 0, f[0]);
+  Frags<C> f[2];
+  if (NACT > 0) read_frags<C, NACT>(L, 0, 0, 0, f[0]);
+  int ca = 0, cb = 0;  // slots of stage kt
   for (int kt = 0; kt < nk; ++kt) {
 #pragma unroll
     for (int ks = 0; ks < kKsteps - 1; ++ks) {
       if (NACT > 0) {
-        read_frags<NACT>(L, kt, ks + 1, f[(ks + 1) & 1]);
-        mfmas<NACT>(f[ks & 1], acc);
+        read_frags<C, NACT>(L, ca, cb, ks + 1, f[(ks + 1) & 1]);
+        mfmas<C, NACT>(f[ks & 1], acc);
         // keep the next k-step's fragment reads spread between this k-step's
         // MFMAs (the machine scheduler would otherwise move reads next to
         // their consumers and expose LDS latency)
-#pragma unroll
-        for (int i = 0; i < NACT + 4; ++i) {
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one DS read
-          __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // two MFMAs
-        }
-        __builtin_amdgcn_sched_group_barrier(0x008, 4 * NACT - 2 * (NACT + 4) > 0 ? 4 * NACT - 2 * (NACT + 4) : 0, 0);
+        interleave<NACT + C::NB, NACT * C::NB>();
       }
     }
     // every fragment of stage kt is in registers, stage kt+1 has landed
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
-    __builtin_amdgcn_s_waitcnt(kWaitVm0);
+    wait_le(loads_after_next<C>(kt, nk));
     bar();
-    if (kt + 2 < nk) issue(kt + 2);
+    if (kt + C::SA < nk) issue_a<C>(L, kt + C::SA, ca);
+    if (kt + C::SB < nk) issue_b<C>(L, kt + C::SB, cb);
+    const int na = ca + 1 == C::SA ? 0 : ca + 1;
+    const int nb = cb + 1 == C::SB ? 0 : cb + 1;
     if (NACT > 0) {
-      if (kt + 1 < nk) read_frags<NACT>(L, kt + 1, 0, f[0]);
-      mfmas<NACT>(f[(kKsteps - 1) & 1], acc);
+      if (kt + 1 < nk) read_frags<C, NACT>(L, na, nb, 0, f[0]);
+      mfmas<C, NACT>(f[(kKsteps - 1) & 1], acc);
+    }
+    ca = na;
+    cb = nb;
+  }
+}
+
+// One work item (m-tile row0.. of group rows ending at row_end, n-tile ni)
+// in tile shape C.
+template <class C, int MODE>
+__device__ __forceinline__ void run_item(const GroupedProblem& p, bf16_t* smem, const bf16_t* A,
+                                         bf16_t* C_out, const bf16_t* Bbase, int row0, int row_end,
+                                         int ni, int K, int wave, int lane) {
+  const int wm = wave / C::WN, wn = wave % C::WN;
+  const int lrow = lane & 31, khalf = lane >> 5;
+  const int lr = lane >> 3, lp = lane & 7;
+  const bf16_t* Atile = A + (size_t)row0 * K;
+  const int a_rows = min(C::BM, p.P - row0);  // rows past it read zeros; their results are discarded
+
+  KLoop kl;
+  kl.smem = smem;
+  kl.ra = buffer_rsrc(Atile, (uint32_t)(a_rows * K * 2));
+  kl.rb = buffer_rsrc(Bbase, (uint32_t)((MODE == MODE_GATEUP ? 2 * p.F : p.H) * K * 2));
+  kl.row_bytes = K * 2;
+  {
+    // swizzle of the wave's first load row of each operand; odd j flips bit 2
+    const int ca = lp ^ ((((C::BM / kWaves) * wave + lr) >> 1) & 7);
+    const int cb = lp ^ ((((BN / kWaves) * wave + lr) >> 1) & 7);
+    kl.a_lane[0] = lr * K * 2 + ca * 16;
+    kl.a_lane[1] = lr * K * 2 + (ca ^ 4) * 16;
+    kl.b_lane[0] = lr * K * 2 + cb * 16;
+    kl.b_lane[1] = lr * K * 2 + (cb ^ 4) * 16;
+    kl.a_row0 = (C::BM / kWaves) * wave;
+#pragma unroll
+    for (int j = 0; j < kBLoads; ++j) {
+      if (MODE == MODE_GATEUP) {
+        // wavefront column wc owns TN/2 gate rows f and the TN/2 matching up
+        // rows F+f, f = ni*128 + wc*TN/2 + q; LDS B row 64 w + 8 j sits in
+        // column (64 w) / TN at position q0 = (64 w) % TN + 8 j
+        const int r = (BN / kWaves) * wave + 8 * j;
+        const int wc = r / C::TN, q = r % C::TN;
+        const int half = C::TN / 2;
+        kl.b_row[j] = ni * (BN / 2) + wc * half + (q < half ? q : q - half + p.F);
+      } else {
+        kl.b_row[j] = ni * BN + (BN / kWaves) * wave + 8 * j;
+      }
+    }
+  }
+  kl.lds_a_load = (C::BM / kWaves) * wave * BK;
+  kl.lds_b_load = (BN / kWaves) * wave * BK;
+  kl.lds_a = (wm * C::TM + lrow) * BK;
+  kl.lds_b = (wn * C::TN + lrow) * BK;
+  kl.sw = (lrow >> 1) & 7;
+  kl.nk = K / BK;
+  kl.khalf = khalf;
+
+  floatx16 acc[C::MB][C::NB];
+#pragma unroll
+  for (int i = 0; i < C::MB; ++i)
+#pragma unroll
+    for (int j = 0; j < C::NB; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  // 32-row blocks of this wave's TM rows that hold rows of the group
+  const int nact = min(C::MB, max(0, (row_end - (row0 + wm * C::TM) + 31) / 32));
+  if constexpr (C::MB == 4) {
+    switch (nact) {
+      case 4: k_loop<C, 4>(kl, acc); break;
+      case 3: k_loop<C, 3>(kl, acc); break;
+      case 2: k_loop<C, 2>(kl, acc); break;
+      case 1: k_loop<C, 1>(kl, acc); break;
+      default: k_loop<C, 0>(kl, acc); break;
+    }
+  } else if constexpr (C::MB == 2) {
+    switch (nact) {
+      case 2: k_loop<C, 2>(kl, acc); break;
+      case 1: k_loop<C, 1>(kl, acc); break;
+      default: k_loop<C, 0>(kl, acc); break;
+    }
+  } else {
+    static_assert(C::MB == 1, "tile shape");
+    if (nact == 1) k_loop<C, 1>(kl, acc); else k_loop<C, 0>(kl, acc);
+  }
+  __syncthreads();  // every wave is done with the ring before the next item refills it
+
+  // epilogue: acc[mb][nb][v] is C[row][col] with col = lane%32 of the 32x32
+  // block and row = 8*(v/4) + 4*(lane/32) + v%4
+#pragma unroll
+  for (int mb = 0; mb < C::MB; ++mb) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int row = row0 + wm * C::TM + mb * 32 + 8 * (v >> 2) + 4 * khalf + (v & 3);
+      if (row >= row_end) continue;
+      if (MODE == MODE_GATEUP) {
+#pragma unroll
+        for (int nb = 0; nb < C::NB / 2; ++nb) {
+          const int f = ni * (BN / 2) + wn * (C::TN / 2) + nb * 32 + lrow;
+          C_out[(size_t)row * p.F + f] = f32_to_bf16(swiglu(acc[mb][nb][v], acc[mb][nb + C::NB / 2][v]));
+        }
+      } else {
+#pragma unroll
+        for (int nb = 0; nb < C::NB; ++nb) {
+          const int n = ni * BN + wn * C::TN + nb * 32 + lrow;
+          C_out[(size_t)row * p.H + n] = f32_to_bf16(acc[mb][nb][v]);
+        }
+      }
     }
   }
 }
 
-// Persistent grouped GEMM.  Work item = (group, n-tile, m-tile), enumerated
-// group by group, n-tile-major, m-tile fastest, so consecutive items share
-// the weight tile.  Workgroup b runs on XCD b % 8 (round-robin dispatch); XCD
-// x walks its own contiguous eighth of the items with its workgroups side by
-// side, so items running together on one L2 share weight and activation
-// tiles.
+// Persistent grouped GEMM.  Work item = (group, n-tile, m-tile of 256 rows),
+// enumerated group by group, n-tile-major, m-tile fastest, so consecutive
+// items share the weight tile.  Workgroup b runs on XCD b % 8 (round-robin
+// dispatch); XCD x walks its own contiguous eighth of the items with its
+// workgroups side by side, so items running together on one L2 share weight
+// and activation tiles.  Each item runs in the tile shape of the rows it
+// holds; all shapes accumulate K in the same order, so a row's result does
+// not depend on the shape it was computed in.
 template <int MODE>
 __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_bf16(GroupedProblem p, WeightTable wt,
                                                                  const bf16_t* __restrict__ A,
                                                                  bf16_t* __restrict__ C,
                                                                  int n_ntiles) {
-  __shared__ __attribute__((aligned(1024))) bf16_t smem[kStages * kStageElems];
+  __shared__ __attribute__((aligned(1024))) bf16_t smem[kLdsElems];
   // the LDS ring is written by global->LDS loads the compiler does not see
   asm volatile("" ::"v"(smem) : "memory");
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
-  const int lrow = lane & 31, khalf = lane >> 5;
   const int xcd = blockIdx.x % kXcds, slot = blockIdx.x / kXcds, nslots = gridDim.x / kXcds;
   const int G = *p.n_groups;
   const long long total = (long long)(*p.n_tiles) * n_ntiles;
   const int lo = (int)((xcd * total) / kXcds), hi = (int)(((xcd + 1) * total) / kXcds);
   const int K = MODE == MODE_GATEUP ? p.H : p.F;
-  const int nk = K / BK;
   const int ES = p.E + p.S;
-
-  const int lr = lane >> 3, lp = lane & 7;  // load slot of this lane (see KLoop)
 
   for (int it = lo + slot; it < hi; it += nslots) {
     // group of this item: the last g with cum_mt[g] * n_ntiles <= it
@@ -229,83 +440,15 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_bf16(GroupedProblem 
     const bf16_t* Bbase = MODE == MODE_GATEUP
         ? static_cast<const bf16_t*>(wt.gu[layer]) + (size_t)e * 2 * p.F * p.H
         : static_cast<const bf16_t*>(wt.dn[layer]) + (size_t)e * p.H * p.F;
-    const bf16_t* Atile = A + (size_t)row0 * K;
-    const int a_last = min(BM, p.P - row0) - 1;  // rows past it read zeros; their results are discarded
-
-    KLoop kl;
-    kl.smem = smem;
-    kl.ra = buffer_rsrc(Atile, (uint32_t)((a_last + 1) * K * 2));
-    kl.rb = buffer_rsrc(Bbase, (uint32_t)((MODE == MODE_GATEUP ? 2 * p.F : p.H) * K * 2));
-    kl.row_bytes = K * 2;
-    {
-      const int r0 = 64 * wave + lr;
-      const int c0 = lp ^ ((r0 >> 1) & 7);
-      int brow0;
-      if (MODE == MODE_GATEUP) {
-        // wave column wc = r / 128 owns 64 gate rows and the 64 matching up
-        // rows: tile row r -> f = ni*128 + wc*64 + r%64, gate row f or up row
-        // F+f.  For r = 64 w + 8 j + l/8: r/128 = w/2 and r%128 >= 64 iff w is odd.
-        brow0 = ni * (BN / 2) + (wave >> 1) * 64 + lr + ((wave & 1) ? p.F : 0);
-      } else {
-        brow0 = ni * BN + r0;
-      }
-      kl.a_lane[0] = r0 * K * 2 + c0 * 16;
-      kl.a_lane[1] = r0 * K * 2 + (c0 ^ 4) * 16;
-      kl.b_lane[0] = brow0 * K * 2 + c0 * 16;
-      kl.b_lane[1] = brow0 * K * 2 + (c0 ^ 4) * 16;
-    }
-    kl.lds_load = 64 * wave * BK;
-    kl.lds_a = (wm * 128 + lrow) * BK;
-    kl.lds_b = (wn * 128 + lrow) * BK;
-    kl.sw = (lrow >> 1) & 7;
-    kl.nk = nk;
-    kl.khalf = khalf;
-
-    floatx16 acc[4][4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
-
-    // 32-row blocks of this wave's 128 rows that hold rows of the group
-    const int nact = min(4, max(0, (row_end - (row0 + wm * 128) + 31) / 32));
-    switch (nact) {
-      case 4: k_loop<4>(kl, acc); break;
-      case 3: k_loop<3>(kl, acc); break;
-      case 2: k_loop<2>(kl, acc); break;
-      case 1: k_loop<1>(kl, acc); break;
-      default: k_loop<0>(kl, acc); break;
-    }
-    __syncthreads();  // every wave is done with the ring before the next item refills it
-
-    // epilogue: acc[mb][nb][v] is C[row][col] with col = lane%32 of the 32x32
-    // block and row = 8*(v/4) + 4*(lane/32) + v%4
-#pragma unroll
-    for (int mb = 0; mb < 4; ++mb) {
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = row0 + wm * 128 + mb * 32 + 8 * (v >> 2) + 4 * khalf + (v & 3);
-        if (row >= row_end) continue;
-        if (MODE == MODE_GATEUP) {
-#pragma unroll
-          for (int nb = 0; nb < 2; ++nb) {
-            const int f = ni * (BN / 2) + wn * 64 + nb * 32 + lrow;
-            C[(size_t)row * p.F + f] = f32_to_bf16(swiglu(acc[mb][nb][v], acc[mb][nb + 2][v]));
-          }
-        } else {
-#pragma unroll
-          for (int nb = 0; nb < 4; ++nb) {
-            const int n = ni * BN + wn * 128 + nb * 32 + lrow;
-            C[(size_t)row * p.H + n] = f32_to_bf16(acc[mb][nb][v]);
-          }
-        }
-      }
-    }
+    const int rows = row_end - row0;
+    if (rows > CfgMid::BM)
+      run_item<CfgBig, MODE>(p, smem, A, C, Bbase, row0, row_end, ni, K, wave, lane);
+    else if (rows > CfgSkinny::BM)
+      run_item<CfgMid, MODE>(p, smem, A, C, Bbase, row0, row_end, ni, K, wave, lane);
+    else
+      run_item<CfgSkinny, MODE>(p, smem, A, C, Bbase, row0, row_end, ni, K, wave, lane);
   }
 }
-
 // ---------------------------------------------------------------------------
 // fp32 path
 constexpr int FBM = 64, FBN = 64, FBK = 16;
