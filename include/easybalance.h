@@ -225,15 +225,18 @@ int easybalance_combine(const eb_model_desc* desc, int32_t n_run, const eb_work*
                         void* stream);
 
 /*
- * Kernel timing for measurement.  Between easybalance_profile_begin() and
- * easybalance_profile_end(), every kernel the library launches is bracketed
- * by HIP events recorded on the stream it is launched on.  profile_end waits
- * for those events and returns, per kernel class EB_K_*, the summed duration
- * in ms (ms_out[EB_NUM_KERNELS]) and the launch count
- * (launches_out[EB_NUM_KERNELS]); both host arrays are nullable.  Process-wide
- * state, guarded by a mutex.
+ * Kernel timing for measurement.  Between easybalance_profile_begin(mask) and
+ * easybalance_profile_end(), every kernel the library launches whose class
+ * EB_K_* has its bit (1u << EB_K_*) set in kernel_mask is bracketed by HIP
+ * events recorded on the stream it is launched on (EB_PROFILE_ALL selects
+ * every class; each event pair adds a little time to the stream, so a caller
+ * timing a whole pass selects only the kernels it needs).  profile_end waits
+ * for those events and returns, per kernel class, the summed duration in ms
+ * (ms_out[EB_NUM_KERNELS]) and the launch count (launches_out[EB_NUM_KERNELS]);
+ * both host arrays are nullable.  Process-wide state, guarded by a mutex.
  */
-int easybalance_profile_begin(void);
+#define EB_PROFILE_ALL ((1u << EB_NUM_KERNELS) - 1u)
+int easybalance_profile_begin(uint32_t kernel_mask);
 int easybalance_profile_end(double* ms_out, int64_t* launches_out);
 
 #ifdef __cplusplus

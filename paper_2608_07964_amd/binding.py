@@ -28,6 +28,7 @@ EB_MAXUTIL_MAX_POOL = 20
 KERNEL_NAMES = ["route_norm", "route_logits", "route_topk", "perm_count", "perm_scan",
                 "perm_scatter", "gateup", "down", "combine", "perm_gather"]
 EB_NUM_KERNELS = len(KERNEL_NAMES)
+EB_PROFILE_ALL = (1 << EB_NUM_KERNELS) - 1
 
 EXPORTS = ["easybalance_version", "easybalance_last_error", "easybalance_route",
            "easybalance_schedule", "easybalance_moe_step_workspace_size", "easybalance_moe_step",
@@ -88,7 +89,7 @@ def lib() -> ctypes.CDLL:
     l.easybalance_combine.restype = ctypes.c_int
     l.easybalance_combine.argtypes = [D, I32, W, P, P, P, P]
     l.easybalance_profile_begin.restype = ctypes.c_int
-    l.easybalance_profile_begin.argtypes = []
+    l.easybalance_profile_begin.argtypes = [ctypes.c_uint32]
     l.easybalance_profile_end.restype = ctypes.c_int
     l.easybalance_profile_end.argtypes = [ctypes.POINTER(ctypes.c_double), I64P]
     _lib = l
@@ -188,8 +189,10 @@ def easybalance_combine(desc, run, n_run, x_list, o, inv, stream=None) -> None:
         ctypes.byref(desc), n_run, run, xs, _ptr(o), _ptr(inv), stream))
 
 
-def easybalance_profile_begin() -> None:
-    _check("easybalance_profile_begin", lib().easybalance_profile_begin())
+def easybalance_profile_begin(kernels=None) -> None:
+    """kernels: iterable of KERNEL_NAMES entries to time (default: all)."""
+    mask = EB_PROFILE_ALL if kernels is None else sum(1 << KERNEL_NAMES.index(k) for k in kernels)
+    _check("easybalance_profile_begin", lib().easybalance_profile_begin(mask))
 
 
 def easybalance_profile_end() -> dict:

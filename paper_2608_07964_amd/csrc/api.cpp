@@ -147,6 +147,7 @@ struct EventPair {
 };
 std::mutex g_prof_mu;
 std::atomic<bool> g_prof_on{false};
+std::atomic<uint32_t> g_prof_mask{0};
 std::vector<EventPair> g_prof_done;
 std::vector<hipEvent_t> g_prof_free;
 thread_local hipEvent_t t_pending = nullptr;
@@ -173,8 +174,9 @@ int set_error(int code, const char* fmt, ...) {
 }
 
 void prof_start(int kind, hipStream_t s) {
-  (void)kind;
-  if (!g_prof_on.load(std::memory_order_relaxed)) return;
+  if (!g_prof_on.load(std::memory_order_relaxed) ||
+      !((g_prof_mask.load(std::memory_order_relaxed) >> kind) & 1u))
+    return;
   std::lock_guard<std::mutex> lk(g_prof_mu);
   t_pending = prof_event();
   if (t_pending && hipEventRecord(t_pending, s) != hipSuccess) {
@@ -333,8 +335,9 @@ int easybalance_combine(const eb_model_desc* desc, int32_t n_run, const eb_work*
                     "combine");
 }
 
-int easybalance_profile_begin(void) {
+int easybalance_profile_begin(uint32_t kernel_mask) {
   std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_prof_mask.store(kernel_mask & EB_PROFILE_ALL);
   for (auto& p : g_prof_done) {
     g_prof_free.push_back(p.start);
     g_prof_free.push_back(p.stop);

@@ -1,12 +1,18 @@
 // Routing of one micro-batch at one layer (Section 2.1: W, I = topk(G(h'))):
-//   norm_router_kernel  E <= 8 (bf16) / E <= 64 (fp32): one wavefront per token computes
-//                       a = dtype(x * r * gain) and z = a Wg^T + bias in one pass
-//                       (Wg stays in L2; lane partial sums, butterfly reductions)
-//   rmsnorm_kernel +    bf16 stacks with E > 8: RMSNorm, then the router GEMM on
-//   router_mfma_kernel  the matrix cores (split-K over the 4 wavefronts)
-//   rmsnorm_kernel +    fp32 stacks with E > 64: RMSNorm, then an LDS-tiled fp32
-//   logits_kernel       VALU GEMM for z
-//   topk_kernel         top-k by wavefront argmax, softmax weights, expert counts
+//   route_token_kernel   E <= 8 (bf16) / E <= 64 (fp32), H <= 8192: one workgroup
+//                        per token computes a = dtype(x * r * gain),
+//                        z = a Wg^T + bias and the top-k with its softmax
+//                        weights
+//   rmsnorm_kernel +     other bf16 stacks: RMSNorm, then the router GEMM on
+//   route_mfma_kernel    the matrix cores (split-K over the 4 wavefronts) and
+//                        the top-k of the workgroup's 32 tokens from an LDS
+//                        logit tile
+//   rmsnorm_kernel +     other fp32 stacks: RMSNorm, an LDS-tiled fp32
+//   logits_kernel +      VALU GEMM for z, then the top-k
+//   topk_kernel
+//   counts_kernel        expert counts of the micro-batch from its picks
+// Every reduction runs in a fixed order, so a token's routing depends on its
+// own inputs only (not on the other tokens of the launch).
 #include <math.h>
 
 #include "eb_internal.h"
@@ -15,9 +21,49 @@
 namespace eb {
 namespace {
 
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float floatx16_t __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+// Sum of squares of row xr (H floats) by one wavefront: lane l adds the float4
+// slices l, l + 64, ... in that order (four slices in flight per iteration);
+// the butterfly leaves the bit-identical total in every lane.
+__device__ __forceinline__ float row_sumsq(const float4* __restrict__ xr, int n4, int lane) {
+  float ss = 0.f;
+  int i = lane;
+  for (; i + 192 < n4; i += 256) {
+    const float4 v0 = xr[i], v1 = xr[i + 64], v2 = xr[i + 128], v3 = xr[i + 192];
+    ss = fmaf(v0.x, v0.x, ss); ss = fmaf(v0.y, v0.y, ss); ss = fmaf(v0.z, v0.z, ss); ss = fmaf(v0.w, v0.w, ss);
+    ss = fmaf(v1.x, v1.x, ss); ss = fmaf(v1.y, v1.y, ss); ss = fmaf(v1.z, v1.z, ss); ss = fmaf(v1.w, v1.w, ss);
+    ss = fmaf(v2.x, v2.x, ss); ss = fmaf(v2.y, v2.y, ss); ss = fmaf(v2.z, v2.z, ss); ss = fmaf(v2.w, v2.w, ss);
+    ss = fmaf(v3.x, v3.x, ss); ss = fmaf(v3.y, v3.y, ss); ss = fmaf(v3.z, v3.z, ss); ss = fmaf(v3.w, v3.w, ss);
+  }
+  for (; i < n4; i += 64) {
+    const float4 v = xr[i];
+    ss = fmaf(v.x, v.x, ss); ss = fmaf(v.y, v.y, ss); ss = fmaf(v.z, v.z, ss); ss = fmaf(v.w, v.w, ss);
+  }
+  return wave_sum(ss);
+}
+
+// Four consecutive normalised values, stored in the stack's dtype.
+__device__ __forceinline__ void store4(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
+__device__ __forceinline__ void store4(bf16_t* p, float4 v) {
+  uint2 u;
+  u.x = (uint32_t)f32_to_bf16(v.x) | ((uint32_t)f32_to_bf16(v.y) << 16);
+  u.y = (uint32_t)f32_to_bf16(v.z) | ((uint32_t)f32_to_bf16(v.w) << 16);
+  *reinterpret_cast<uint2*>(p) = u;
+}
+__device__ __forceinline__ float4 normed(float4 v, float r, float4 g) {
+  return make_float4(v.x * r * g.x, v.y * r * g.y, v.z * r * g.z, v.w * r * g.w);
+}
+
 // ---------------------------------------------------------------------------
-// RMSNorm + cast.  Each lane sums its strided float4 slices in a fixed order;
-// the butterfly reduction leaves the bit-identical total in every lane.
+// RMSNorm + cast, one wavefront per token.
 template <typename TA>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(int T, int H, const float* __restrict__ x,
                                                       const float* __restrict__ gain,
@@ -28,26 +74,161 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(int T, int H, const float*
   const float4* xr = reinterpret_cast<const float4*>(x + (size_t)t * H);
   const float4* g4 = reinterpret_cast<const float4*>(gain);
   const int n4 = H >> 2;
-  float ss = 0.f;
-  for (int i = lane; i < n4; i += 64) {
-    const float4 v = xr[i];
-    ss = fmaf(v.x, v.x, ss);
-    ss = fmaf(v.y, v.y, ss);
-    ss = fmaf(v.z, v.z, ss);
-    ss = fmaf(v.w, v.w, ss);
+  const float r = 1.0f / sqrtf(row_sumsq(xr, n4, lane) / (float)H + eps);
+  TA* ar = a + (size_t)t * H;
+  int i = lane;
+  for (; i + 192 < n4; i += 256) {
+    const float4 v0 = xr[i], v1 = xr[i + 64], v2 = xr[i + 128], v3 = xr[i + 192];
+    const float4 g0 = g4[i], g1 = g4[i + 64], g2 = g4[i + 128], g3 = g4[i + 192];
+    store4(ar + 4 * i, normed(v0, r, g0));
+    store4(ar + 4 * (i + 64), normed(v1, r, g1));
+    store4(ar + 4 * (i + 128), normed(v2, r, g2));
+    store4(ar + 4 * (i + 192), normed(v3, r, g3));
+  }
+  for (; i < n4; i += 64) store4(ar + 4 * i, normed(xr[i], r, g4[i]));
+}
+
+// ---------------------------------------------------------------------------
+// Top-k and softmax weights of one token by one thread.  zrow(e) gives the
+// token's logits e < E.  The picks are kept as a list ordered by the total
+// order "larger z first, then lower expert id" (NaN is never picked; a slot
+// that nothing can fill takes expert E-1), built by one ascending pass over e
+// with compare-and-swap insertion; the softmax maximum and denominator are
+// accumulated over e in ascending order.
+__device__ __forceinline__ bool better(float v1, int e1, float v2, int e2) {
+  return v1 > v2 || (v1 == v2 && e1 < e2);
+}
+
+template <int KMAX, class ZRow>
+__device__ __forceinline__ void topk_thread(int E, int k, int norm_topk, ZRow zrow,
+                                            int32_t* __restrict__ idx_t, float* __restrict__ w_t) {
+  float lv[KMAX];
+  int le[KMAX];
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) {
+    lv[j] = -INFINITY;
+    le[j] = E;  // sentinel: loses to every expert
+  }
+  float mx = -INFINITY;
+  for (int e = 0; e < E; ++e) {
+    float v = zrow(e);
+    mx = fmaxf(mx, v);
+    int ve = e;
+#pragma unroll
+    for (int j = 0; j < KMAX; ++j) {
+      if (j < k && better(v, ve, lv[j], le[j])) {
+        const float tv = lv[j];
+        const int te = le[j];
+        lv[j] = v;
+        le[j] = ve;
+        v = tv;
+        ve = te;
+      }
+    }
+  }
+  float se = 0.f;
+  for (int e = 0; e < E; ++e) se += expf(zrow(e) - mx);
+  float ev[KMAX], esum = 0.f;
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) {
+    ev[j] = j < k ? expf(lv[j] - mx) : 0.f;
+    esum += ev[j];
+  }
+  const float denom = norm_topk ? esum : se;
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) {
+    if (j < k) {
+      idx_t[j] = le[j] < E ? le[j] : E - 1;
+      w_t[j] = ev[j] / denom;
+    }
+  }
+}
+
+// Dispatch on k: KMAX = 8 for k <= 8, else 16.
+template <class ZRow>
+__device__ __forceinline__ void topk_token(int E, int k, int norm_topk, ZRow zrow,
+                                           int32_t* __restrict__ idx_t, float* __restrict__ w_t) {
+  if (k <= 8) topk_thread<8>(E, k, norm_topk, zrow, idx_t, w_t);
+  else topk_thread<16>(E, k, norm_topk, zrow, idx_t, w_t);
+}
+
+// Top-k and softmax weights of one token by 8 consecutive lanes (sub = lane
+// % 8): lane sub holds the logits e = sub + 8 i (i < PER) and each pick is an
+// argmax over the 8 lanes' local bests under the same total order; the
+// softmax maximum and denominator are reduced over the 8 lanes in a fixed
+// pattern.  Lane sub 0 writes idx_t and w_t.
+template <int PER>
+__device__ __forceinline__ void topk_group8(int sub, int E, int k, int norm_topk, const float* zrow,
+                                            int32_t* __restrict__ idx_t, float* __restrict__ w_t) {
+  static_assert(PER <= 32, "taken mask");
+  float v[PER];
+  uint32_t taken = 0;
+  float mx = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int e = sub + 8 * i;
+    if (e < E) {
+      v[i] = zrow[e];
+      mx = fmaxf(mx, v[i]);
+    } else {
+      v[i] = -INFINITY;
+      taken |= 1u << i;
+    }
   }
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off, 64);
-  const float r = 1.0f / sqrtf(ss / (float)H + eps);
-  TA* ar = a + (size_t)t * H;
-  for (int i = lane; i < n4; i += 64) {
-    const float4 v = xr[i];
-    const float4 g = g4[i];
-    Elem<TA>::store(ar, 4 * i + 0, v.x * r * g.x);
-    Elem<TA>::store(ar, 4 * i + 1, v.y * r * g.y);
-    Elem<TA>::store(ar, 4 * i + 2, v.z * r * g.z);
-    Elem<TA>::store(ar, 4 * i + 3, v.w * r * g.w);
+  for (int off = 1; off < 8; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 8));
+  float se = 0.f;
+#pragma unroll
+  for (int i = 0; i < PER; ++i)
+    if (!(taken & (1u << i))) se += expf(v[i] - mx);
+#pragma unroll
+  for (int off = 1; off < 8; off <<= 1) se += __shfl_xor(se, off, 8);
+  float esum = 0.f;
+  for (int r = 0; r < k; ++r) {
+    float bv = -INFINITY;
+    int be = E;  // sentinel: nothing selectable in this lane
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int e = sub + 8 * i;
+      if (!(taken & (1u << i)) && better(v[i], e, bv, be)) {
+        bv = v[i];
+        be = e;
+      }
+    }
+#pragma unroll
+    for (int off = 1; off < 8; off <<= 1) {
+      const float ov = __shfl_xor(bv, off, 8);
+      const int oe = __shfl_xor(be, off, 8);
+      if (better(ov, oe, bv, be)) {
+        bv = ov;
+        be = oe;
+      }
+    }
+    if (be >= E) be = E - 1;  // only when every remaining logit is NaN
+    if ((be & 7) == sub) taken |= 1u << (be >> 3);
+    const float ev = expf(bv - mx);
+    esum += ev;
+    if (sub == 0) {
+      idx_t[r] = be;
+      w_t[r] = ev;
+    }
   }
+  if (sub == 0) {
+    const float denom = norm_topk ? esum : se;
+    for (int r = 0; r < k; ++r) w_t[r] = w_t[r] / denom;
+  }
+}
+
+// Expert counts of the micro-batch from its picks, by one workgroup (an LDS
+// histogram, then one plain store per expert: nothing to clear beforehand).
+__global__ __launch_bounds__(1024) void counts_kernel(int n, int E, const int32_t* __restrict__ idx,
+                                                      int32_t* __restrict__ counts) {
+  __shared__ int hist[1024];
+  for (int e = threadIdx.x; e < E; e += blockDim.x) hist[e] = 0;
+  __syncthreads();
+  for (int i = threadIdx.x; i < n; i += blockDim.x) atomicAdd(&hist[idx[i]], 1);
+  __syncthreads();
+  for (int e = threadIdx.x; e < E; e += blockDim.x) counts[e] = hist[e];
 }
 
 // ---------------------------------------------------------------------------
@@ -107,88 +288,152 @@ __global__ __launch_bounds__(256) void logits_kernel(int T, int H, int E, const 
 }
 
 // ---------------------------------------------------------------------------
-// Fused RMSNorm + router logits for E <= EMAX.  Lane l owns the 8-element
-// chunks starting at h = 8 (l + 64 i); per chunk it forms the stored a values and adds
-// their products with every router row into one accumulator per expert; each
-// expert's lane partial sums are then reduced by a butterfly (bit-identical
-// total in every lane) and lane e writes z[t][e].
+// Whole routing of one token for E <= EMAX by one workgroup of 256 threads.
+// Thread tid owns the 8-element chunks starting at h = 8 (tid + 256 i), held
+// in registers; per chunk it forms and stores the a values and adds their
+// (stored, rounded) values times every router row into one accumulator per
+// expert.  Sums of squares and logits are reduced by a butterfly per
+// wavefront and then over the 4 wavefronts in order; wavefront 0 adds the
+// bias and picks the top-k.
+template <typename TA> struct Vec8;
+template <> struct Vec8<bf16_t> {
+  // 8 bf16 of a router row / of a
+  __device__ static __forceinline__ void load(const bf16_t* p, float (&f)[8]) {
+    const uint4 u = *reinterpret_cast<const uint4*>(p);
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      f[2 * q] = __uint_as_float(w[q] << 16);
+      f[2 * q + 1] = __uint_as_float(w[q] & 0xffff0000u);
+    }
+  }
+  // stores dtype(v) and replaces v by it
+  __device__ static __forceinline__ void store_round(bf16_t* p, float (&v)[8]) {
+    uint32_t w[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const bf16_t lo = f32_to_bf16(v[2 * q]), hi = f32_to_bf16(v[2 * q + 1]);
+      w[q] = (uint32_t)lo | ((uint32_t)hi << 16);
+      v[2 * q] = bf16_to_f32(lo);
+      v[2 * q + 1] = bf16_to_f32(hi);
+    }
+    *reinterpret_cast<uint4*>(p) = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+};
+template <> struct Vec8<float> {
+  __device__ static __forceinline__ void load(const float* p, float (&f)[8]) {
+    const float4 u = reinterpret_cast<const float4*>(p)[0], v = reinterpret_cast<const float4*>(p)[1];
+    f[0] = u.x; f[1] = u.y; f[2] = u.z; f[3] = u.w; f[4] = v.x; f[5] = v.y; f[6] = v.z; f[7] = v.w;
+  }
+  __device__ static __forceinline__ void store_round(float* p, float (&v)[8]) {
+    reinterpret_cast<float4*>(p)[0] = make_float4(v[0], v[1], v[2], v[3]);
+    reinterpret_cast<float4*>(p)[1] = make_float4(v[4], v[5], v[6], v[7]);
+  }
+};
+
+constexpr int kTokChunks = 4;  // 8-element chunks per thread: H <= 256 * 8 * 4
+constexpr int kTokMaxH = 256 * 8 * kTokChunks;
+
 template <typename TA, int EMAX>
-__global__ __launch_bounds__(256) void norm_router_kernel(int T, int H, int E, const float* __restrict__ x,
-                                                          const float* __restrict__ gain,
-                                                          const TA* __restrict__ Wg,
-                                                          const float* __restrict__ bias,
-                                                          TA* __restrict__ a, float* __restrict__ z,
-                                                          float eps) {
-  const int lane = threadIdx.x & 63;
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= T) return;
+__global__ __launch_bounds__(256) void route_token_kernel(
+    int T, int H, int E, int k, int norm_topk, const float* __restrict__ x,
+    const float* __restrict__ gain, const TA* __restrict__ Wg, const float* __restrict__ bias,
+    TA* __restrict__ a, float* __restrict__ z, int32_t* __restrict__ idx, float* __restrict__ w,
+    float eps) {
+  __shared__ float red[4];
+  __shared__ float red_z[4][EMAX + 1];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int t = blockIdx.x;
   const float* xr = x + (size_t)t * H;
-  const int nchunk = H >> 3;  // 8-element chunks; lane l takes chunks l, l + 64, ...
+  const int nchunk = H >> 3;
+  // thread tid owns chunks c = tid + 256 i (8 elements each), kept in registers
+  float xs[kTokChunks][8];
   float ss = 0.f;
-  for (int c = lane; c < nchunk; c += 64) {
-    const float4* p4 = reinterpret_cast<const float4*>(xr + 8 * c);
-    const float4 u = p4[0], v = p4[1];
-    ss = fmaf(u.x, u.x, ss); ss = fmaf(u.y, u.y, ss); ss = fmaf(u.z, u.z, ss); ss = fmaf(u.w, u.w, ss);
-    ss = fmaf(v.x, v.x, ss); ss = fmaf(v.y, v.y, ss); ss = fmaf(v.z, v.z, ss); ss = fmaf(v.w, v.w, ss);
+#pragma unroll
+  for (int i = 0; i < kTokChunks; ++i) {
+    const int c = tid + 256 * i;
+    if (c < nchunk) {
+      const float4 u = reinterpret_cast<const float4*>(xr + 8 * c)[0];
+      const float4 v = reinterpret_cast<const float4*>(xr + 8 * c)[1];
+      xs[i][0] = u.x; xs[i][1] = u.y; xs[i][2] = u.z; xs[i][3] = u.w;
+      xs[i][4] = v.x; xs[i][5] = v.y; xs[i][6] = v.z; xs[i][7] = v.w;
+    }
   }
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off, 64);
-  const float r = 1.0f / sqrtf(ss / (float)H + eps);
+  for (int i = 0; i < kTokChunks; ++i)
+    if (tid + 256 * i < nchunk)
+#pragma unroll
+      for (int q = 0; q < 8; ++q) ss = fmaf(xs[i][q], xs[i][q], ss);
+  ss = wave_sum(ss);
+  if (lane == 0) red[wave] = ss;
+  __syncthreads();
+  const float r = 1.0f / sqrtf((((red[0] + red[1]) + red[2]) + red[3]) / (float)H + eps);
   float acc[EMAX];
 #pragma unroll
   for (int e = 0; e < EMAX; ++e) acc[e] = 0.f;
   TA* ar = a + (size_t)t * H;
-  for (int c = lane; c < nchunk; c += 64) {
-    const int h = 8 * c;
-    const float4* p4 = reinterpret_cast<const float4*>(xr + h);
-    const float4* g4 = reinterpret_cast<const float4*>(gain + h);
-    const float4 u = p4[0], v = p4[1], gu = g4[0], gv = g4[1];
-    float av[8] = {u.x * r * gu.x, u.y * r * gu.y, u.z * r * gu.z, u.w * r * gu.w,
-                   v.x * r * gv.x, v.y * r * gv.y, v.z * r * gv.z, v.w * r * gv.w};
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      Elem<TA>::store(ar, h + q, av[q]);
-      av[q] = Elem<TA>::round(av[q]);  // the stored (rounded) value feeds the router
-    }
+  for (int i = 0; i < kTokChunks; ++i) {
+    const int c = tid + 256 * i;
+    if (c < nchunk) {
+      const int h = 8 * c;
+      const float4 gu = reinterpret_cast<const float4*>(gain + h)[0];
+      const float4 gv = reinterpret_cast<const float4*>(gain + h)[1];
+      const float g[8] = {gu.x, gu.y, gu.z, gu.w, gv.x, gv.y, gv.z, gv.w};
+      float av[8];
 #pragma unroll
-    for (int e = 0; e < EMAX; ++e) {
-      if (e < E) {
-        const TA* wr = Wg + (size_t)e * H + h;
+      for (int q = 0; q < 8; ++q) av[q] = xs[i][q] * r * g[q];
+      Vec8<TA>::store_round(ar + h, av);  // the stored (rounded) values feed the router
 #pragma unroll
-        for (int q = 0; q < 8; ++q) acc[e] = fmaf(av[q], Elem<TA>::load(wr, q), acc[e]);
+      for (int e = 0; e < EMAX; ++e) {
+        if (e < E) {
+          float wv[8];
+          Vec8<TA>::load(Wg + (size_t)e * H + h, wv);
+#pragma unroll
+          for (int q = 0; q < 8; ++q) acc[e] = fmaf(av[q], wv[q], acc[e]);
+        }
       }
     }
   }
 #pragma unroll
   for (int e = 0; e < EMAX; ++e) {
     if (e < E) {
-      float v = acc[e];
-#pragma unroll
-      for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-      if (lane == e) z[(size_t)t * E + e] = v + bias[e];
+      const float v = wave_sum(acc[e]);
+      if (lane == 0) red_z[wave][e] = v;
     }
   }
+  __syncthreads();
+  if (tid < E) {
+    const float ze = (((red_z[0][tid] + red_z[1][tid]) + red_z[2][tid]) + red_z[3][tid]) + bias[tid];
+    red_z[0][tid] = ze;  // each thread rewrites only its own entry
+    z[(size_t)t * E + tid] = ze;
+  }
+  __syncthreads();
+  if (tid == 0)
+    topk_token(E, k, norm_topk, [&](int e) { return red_z[0][e]; }, idx + (size_t)t * k,
+               w + (size_t)t * k);
 }
 
 // ---------------------------------------------------------------------------
-// Router logits on the matrix cores (bf16 stacks, 8 < E <= 256):
-// z[T][E] = a Wg^T + bias.  A workgroup takes 32 tokens and all experts
-// (padded to NB blocks of 32); its 4 wavefronts split K into quarters, each
-// accumulating a 32 x 32 NB partial with v_mfma_f32_32x32x16_bf16 from
-// operands loaded straight from L2 into registers (one 32-wide K chunk
-// prefetched).  Waves 1..3 leave their partials in LDS and wave 0 adds them in
-// that order, then adds the bias: a fixed summation order, so the logits of a
-// micro-batch do not depend on anything but its inputs.
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef float floatx16_t __attribute__((ext_vector_type(16)));
-
+// Router logits on the matrix cores and top-k (bf16 stacks, E <= 256).
+// A workgroup takes 32 tokens and all experts (padded to NB blocks of 32);
+// its 4 wavefronts split K into quarters, each accumulating a 32 x 32 NB
+// partial with v_mfma_f32_32x32x16_bf16 from operands loaded straight from L2
+// into registers (a ring of 32-wide K chunks in flight).  Waves 1..3 leave their
+// partials in LDS and wave 0 adds them in that order, then the bias (a fixed
+// summation order), and writes the logits to z and to an LDS tile from which
+// 8 lanes per token pick its top-k.
 template <int NB>
-__global__ __launch_bounds__(256) void router_mfma_kernel(int T, int H, int E,
-                                                          const bf16_t* __restrict__ a,
-                                                          const bf16_t* __restrict__ Wg,
-                                                          const float* __restrict__ bias,
-                                                          float* __restrict__ z) {
+__global__ __launch_bounds__(256) void route_mfma_kernel(int T, int H, int E, int k, int norm_topk,
+                                                         const bf16_t* __restrict__ a,
+                                                         const bf16_t* __restrict__ Wg,
+                                                         const float* __restrict__ bias,
+                                                         float* __restrict__ z,
+                                                         int32_t* __restrict__ idx,
+                                                         float* __restrict__ w) {
+  constexpr int ZS = NB * 32 + 1;  // padded LDS row of the logit tile
   __shared__ float part[3][NB][16][64];
+  __shared__ float zs[32][ZS];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lrow = lane & 31, khalf = lane >> 5;
   const int t0 = blockIdx.x * 32;
@@ -204,15 +449,16 @@ __global__ __launch_bounds__(256) void router_mfma_kernel(int T, int H, int E,
   for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
     for (int v = 0; v < 16; ++v) acc[nb][v] = 0.f;
-  // a 32-wide K chunk = two MFMA k-steps of 16
-  bf16x8_t ac[2][2], bc[2][NB][2];
-  auto load = [&](int buf, int k) {
+  // a 32-wide K chunk = two MFMA k-steps of 16; a ring of D chunks in flight
+  constexpr int D = NB <= 4 ? 4 : 2;
+  bf16x8_t ac[D][2], bc[D][NB][2];
+  auto load = [&](int buf, int kk) {
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
-      ac[buf][s] = *reinterpret_cast<const bf16x8_t*>(arow + k + 16 * s);
+      ac[buf][s] = *reinterpret_cast<const bf16x8_t*>(arow + kk + 16 * s);
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
-        bc[buf][nb][s] = *reinterpret_cast<const bf16x8_t*>(brow[nb] + k + 16 * s);
+        bc[buf][nb][s] = *reinterpret_cast<const bf16x8_t*>(brow[nb] + kk + 16 * s);
     }
   };
   auto mma = [&](int buf) {
@@ -222,12 +468,19 @@ __global__ __launch_bounds__(256) void router_mfma_kernel(int T, int H, int E,
       for (int nb = 0; nb < NB; ++nb)
         acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ac[buf][s], bc[buf][nb][s], acc[nb], 0, 0, 0);
   };
-  load(0, 0);
-  for (int k = 0; k < kq; k += 64) {
-    if (k + 32 < kq) load(1, k + 32);
-    mma(0);
-    if (k + 64 < kq) load(0, k + 64);
-    if (k + 32 < kq) mma(1);
+  const int nch = kq / 32;
+#pragma unroll
+  for (int d = 0; d < D; ++d)
+    if (d < nch) load(d, 32 * d);
+  for (int c0 = 0; c0 < nch; c0 += D) {
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      const int c = c0 + d;
+      if (c < nch) {
+        mma(d);
+        if (c + D < nch) load(d, 32 * (c + D));
+      }
+    }
   }
   if (wave > 0) {
 #pragma unroll
@@ -236,107 +489,44 @@ __global__ __launch_bounds__(256) void router_mfma_kernel(int T, int H, int E,
       for (int v = 0; v < 16; ++v) part[wave - 1][nb][v][lane] = acc[nb][v];
   }
   __syncthreads();
-  if (wave != 0) return;
+  if (wave == 0) {
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
+    for (int nb = 0; nb < NB; ++nb) {
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      float sum = acc[nb][v];
+      for (int v = 0; v < 16; ++v) {
+        float sum = acc[nb][v];
 #pragma unroll
-      for (int w = 0; w < 3; ++w) sum += part[w][nb][v][lane];
-      // C[row][col]: col = lane % 32 of block nb (expert), row = 8 (v/4) + 4 (lane/32) + v%4 (token)
-      const int t = t0 + 8 * (v >> 2) + 4 * khalf + (v & 3);
-      const int e = nb * 32 + lrow;
-      if (t < T && e < E) z[(size_t)t * E + e] = sum + bias[e];
+        for (int q = 0; q < 3; ++q) sum += part[q][nb][v][lane];
+        // C[row][col]: col = lane % 32 of block nb (expert), row = 8 (v/4) + 4 (lane/32) + v%4 (token)
+        const int tl = 8 * (v >> 2) + 4 * khalf + (v & 3);
+        const int e = nb * 32 + lrow;
+        if (e < E) {
+          const float ze = sum + bias[e];
+          zs[tl][e] = ze;
+          if (t0 + tl < T) z[(size_t)(t0 + tl) * E + e] = ze;
+        }
+      }
     }
   }
+  __syncthreads();
+  // 8 lanes per token
+  const int tl = threadIdx.x >> 3, t = t0 + tl;
+  if (t < T)
+    topk_group8<NB * 4>(threadIdx.x & 7, E, k, norm_topk, zs[tl], idx + (size_t)t * k,
+                        w + (size_t)t * k);
 }
 
 // ---------------------------------------------------------------------------
-// Top-k, softmax weights and expert counts.  One wavefront per token; lane l
-// holds logits e = l + 64 s.  Each pick is a wavefront argmax under the total
-// order (larger z first, then lower expert id), so every lane agrees.
-constexpr int TK_MAX_PER_LANE = 16;  // E <= 1024
-
-__device__ __forceinline__ bool better(float v1, int e1, float v2, int e2) {
-  return v1 > v2 || (v1 == v2 && e1 < e2);
-}
-
+// Top-k from logits in global memory (fp32 stacks without the fused path),
+// one thread per token.
 __global__ __launch_bounds__(256) void topk_kernel(int T, int E, int k, int norm_topk,
                                                    const float* __restrict__ z,
                                                    int32_t* __restrict__ idx,
-                                                   float* __restrict__ w,
-                                                   int32_t* __restrict__ counts) {
-  __shared__ int hist[1024];
-  for (int e = threadIdx.x; e < E; e += blockDim.x) hist[e] = 0;
-  __syncthreads();
-  const int lane = threadIdx.x & 63;
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t < T) {
-    const int per = (E + 63) >> 6;
-    float v[TK_MAX_PER_LANE];
-    uint32_t taken = 0;
-    float mx = -INFINITY;
-#pragma unroll
-    for (int s = 0; s < TK_MAX_PER_LANE; ++s) {
-      const int e = lane + 64 * s;
-      if (s < per && e < E) {
-        v[s] = z[(size_t)t * E + e];
-        mx = fmaxf(mx, v[s]);
-      } else {
-        v[s] = -INFINITY;
-        taken |= 1u << s;
-      }
-    }
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
-    float se = 0.f;
-#pragma unroll
-    for (int s = 0; s < TK_MAX_PER_LANE; ++s)
-      if (!(taken & (1u << s))) se += expf(v[s] - mx);
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) se += __shfl_xor(se, off, 64);
-    // picks and unnormalised weights go straight to the outputs (lane 0);
-    // the weights are divided by the softmax denominator afterwards
-    float esum = 0.f;
-    for (int r = 0; r < k; ++r) {
-      float bv = -INFINITY;
-      int be = E;  // sentinel: nothing selectable in this lane
-#pragma unroll
-      for (int s = 0; s < TK_MAX_PER_LANE; ++s) {
-        const int e = lane + 64 * s;
-        if (!(taken & (1u << s)) && better(v[s], e, bv, be)) {
-          bv = v[s];
-          be = e;
-        }
-      }
-#pragma unroll
-      for (int off = 32; off > 0; off >>= 1) {
-        const float ov = __shfl_xor(bv, off, 64);
-        const int oe = __shfl_xor(be, off, 64);
-        if (better(ov, oe, bv, be)) {
-          bv = ov;
-          be = oe;
-        }
-      }
-      if (be >= E) be = E - 1;  // only when every remaining logit is NaN
-      if ((be & 63) == lane) taken |= 1u << (be >> 6);
-      const float ev = expf(bv - mx);
-      esum += ev;
-      if (lane == 0) {
-        idx[(size_t)t * k + r] = be;
-        w[(size_t)t * k + r] = ev;
-        atomicAdd(&hist[be], 1);
-      }
-    }
-    if (lane == 0) {
-      const float denom = norm_topk ? esum : se;
-      for (int r = 0; r < k; ++r) w[(size_t)t * k + r] = w[(size_t)t * k + r] / denom;
-    }
-  }
-  __syncthreads();
-  for (int e = threadIdx.x; e < E; e += blockDim.x)
-    if (hist[e]) atomicAdd(&counts[e], hist[e]);
+                                                   float* __restrict__ w) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= T) return;
+  const float* zr = z + (size_t)t * E;
+  topk_token(E, k, norm_topk, [&](int e) { return zr[e]; }, idx + (size_t)t * k, w + (size_t)t * k);
 }
 
 __global__ void zero_i32_kernel(int32_t* p, int n) {
@@ -348,36 +538,21 @@ template <typename TA>
 hipError_t route_typed(const eb_model_desc& d, int T, const float* x, const float* gain,
                        const void* Wg, const float* bias, void* a_out, float* logits,
                        int32_t* idx, float* w, int32_t* counts, hipStream_t s) {
-  hipLaunchKernelGGL(zero_i32_kernel, dim3((d.E + 255) / 256), dim3(256), 0, s, counts, d.E);
-  if (T == 0) return hipGetLastError();
-  if (sizeof(TA) == 2 && d.E > 8) {
-    // RMSNorm, then the router GEMM on the matrix cores
-    prof_start(EB_K_ROUTE_NORM, s);
-    hipLaunchKernelGGL(rmsnorm_kernel<TA>, dim3((T + 3) / 4), dim3(256), 0, s, T, d.H, x, gain,
-                       static_cast<TA*>(a_out), d.rms_eps);
-    prof_stop(EB_K_ROUTE_NORM, s);
-    prof_start(EB_K_ROUTE_LOGITS, s);
-    const dim3 grid((T + 31) / 32);
-    const bf16_t* ab = static_cast<const bf16_t*>(a_out);
-    const bf16_t* wb = static_cast<const bf16_t*>(Wg);
-    const int nb = (d.E + 31) / 32;
-    if (nb <= 2)
-      hipLaunchKernelGGL(router_mfma_kernel<2>, grid, dim3(256), 0, s, T, d.H, d.E, ab, wb, bias, logits);
-    else if (nb <= 4)
-      hipLaunchKernelGGL(router_mfma_kernel<4>, grid, dim3(256), 0, s, T, d.H, d.E, ab, wb, bias, logits);
-    else
-      hipLaunchKernelGGL(router_mfma_kernel<8>, grid, dim3(256), 0, s, T, d.H, d.E, ab, wb, bias, logits);
-    prof_stop(EB_K_ROUTE_LOGITS, s);
-  } else if (d.E <= 64) {
+  if (T == 0) {
+    hipLaunchKernelGGL(zero_i32_kernel, dim3((d.E + 255) / 256), dim3(256), 0, s, counts, d.E);
+    return hipGetLastError();
+  }
+  const bool fused_token = (sizeof(TA) == 2 ? d.E <= 8 : d.E <= 64) && d.H <= kTokMaxH;
+  if (fused_token) {
     prof_start(EB_K_ROUTE_LOGITS, s);
     if (d.E <= 8)
-      hipLaunchKernelGGL((norm_router_kernel<TA, 8>), dim3((T + 3) / 4), dim3(256), 0, s, T, d.H, d.E,
-                         x, gain, static_cast<const TA*>(Wg), bias, static_cast<TA*>(a_out), logits,
-                         d.rms_eps);
+      hipLaunchKernelGGL((route_token_kernel<TA, 8>), dim3(T), dim3(256), 0, s, T, d.H, d.E, d.k,
+                         d.norm_topk, x, gain, static_cast<const TA*>(Wg), bias,
+                         static_cast<TA*>(a_out), logits, idx, w, d.rms_eps);
     else
-      hipLaunchKernelGGL((norm_router_kernel<TA, 64>), dim3((T + 3) / 4), dim3(256), 0, s, T, d.H,
-                         d.E, x, gain, static_cast<const TA*>(Wg), bias, static_cast<TA*>(a_out),
-                         logits, d.rms_eps);
+      hipLaunchKernelGGL((route_token_kernel<TA, 64>), dim3(T), dim3(256), 0, s, T, d.H, d.E, d.k,
+                         d.norm_topk, x, gain, static_cast<const TA*>(Wg), bias,
+                         static_cast<TA*>(a_out), logits, idx, w, d.rms_eps);
     prof_stop(EB_K_ROUTE_LOGITS, s);
   } else {
     prof_start(EB_K_ROUTE_NORM, s);
@@ -385,14 +560,34 @@ hipError_t route_typed(const eb_model_desc& d, int T, const float* x, const floa
                        static_cast<TA*>(a_out), d.rms_eps);
     prof_stop(EB_K_ROUTE_NORM, s);
     prof_start(EB_K_ROUTE_LOGITS, s);
-    hipLaunchKernelGGL(logits_kernel<TA>, dim3((T + LG_BT - 1) / LG_BT, (d.E + LG_BE - 1) / LG_BE),
-                       dim3(256), 0, s, T, d.H, d.E, static_cast<const TA*>(a_out),
-                       static_cast<const TA*>(Wg), bias, logits);
-    prof_stop(EB_K_ROUTE_LOGITS, s);
+    if (sizeof(TA) == 2) {
+      const dim3 grid((T + 31) / 32);
+      const bf16_t* ab = static_cast<const bf16_t*>(a_out);
+      const bf16_t* wb = static_cast<const bf16_t*>(Wg);
+      const int nb = (d.E + 31) / 32;
+      if (nb <= 2)
+        hipLaunchKernelGGL(route_mfma_kernel<2>, grid, dim3(256), 0, s, T, d.H, d.E, d.k,
+                           d.norm_topk, ab, wb, bias, logits, idx, w);
+      else if (nb <= 4)
+        hipLaunchKernelGGL(route_mfma_kernel<4>, grid, dim3(256), 0, s, T, d.H, d.E, d.k,
+                           d.norm_topk, ab, wb, bias, logits, idx, w);
+      else
+        hipLaunchKernelGGL(route_mfma_kernel<8>, grid, dim3(256), 0, s, T, d.H, d.E, d.k,
+                           d.norm_topk, ab, wb, bias, logits, idx, w);
+      prof_stop(EB_K_ROUTE_LOGITS, s);
+    } else {
+      hipLaunchKernelGGL(logits_kernel<TA>, dim3((T + LG_BT - 1) / LG_BT, (d.E + LG_BE - 1) / LG_BE),
+                         dim3(256), 0, s, T, d.H, d.E, static_cast<const TA*>(a_out),
+                         static_cast<const TA*>(Wg), bias, logits);
+      prof_stop(EB_K_ROUTE_LOGITS, s);
+      prof_start(EB_K_ROUTE_TOPK, s);
+      hipLaunchKernelGGL(topk_kernel, dim3((T + 255) / 256), dim3(256), 0, s, T, d.E, d.k,
+                         d.norm_topk, logits, idx, w);
+      prof_stop(EB_K_ROUTE_TOPK, s);
+    }
   }
   prof_start(EB_K_ROUTE_TOPK, s);
-  hipLaunchKernelGGL(topk_kernel, dim3((T + 3) / 4), dim3(256), 0, s, T, d.E, d.k, d.norm_topk,
-                     logits, idx, w, counts);
+  hipLaunchKernelGGL(counts_kernel, dim3(1), dim3(1024), 0, s, T * d.k, d.E, idx, counts);
   prof_stop(EB_K_ROUTE_TOPK, s);
   return hipGetLastError();
 }
