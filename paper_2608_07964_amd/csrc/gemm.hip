@@ -217,12 +217,13 @@ __device__ __forceinline__ void read_frags(const KLoop& L, int slot_a, int slot_
   const int chunk = ((ks * 2 + L.khalf) ^ L.sw) * 8;
   const bf16_t* ba = L.smem + slot_a * C::A_ELEMS + chunk;
   const bf16_t* bb = L.smem + C::B_RING + slot_b * C::B_ELEMS + chunk;
-#pragma unroll
-  for (int mb = 0; mb < NACT; ++mb)
-    f.a[mb] = *reinterpret_cast<const bf16x8*>(ba + L.lds_a + mb * 32 * BK);
+  // issued in the order the next k-step's MFMAs (mb-major) consume them
 #pragma unroll
   for (int nb = 0; nb < C::NB; ++nb)
     f.b[nb] = *reinterpret_cast<const bf16x8*>(bb + L.lds_b + nb * 32 * BK);
+#pragma unroll
+  for (int mb = 0; mb < NACT; ++mb)
+    f.a[mb] = *reinterpret_cast<const bf16x8*>(ba + L.lds_a + mb * 32 * BK);
 }
 
 template <class C, int NACT>
