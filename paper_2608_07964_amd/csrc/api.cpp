@@ -65,7 +65,7 @@ StepShape step_shape(const eb_model_desc& d, int n_run, const int32_t* T) {
 }
 
 struct WsLayout {
-  size_t hist, chunk_base, offsets, tiles, n_tiles, groups, n_groups, perm, a_perm, h, total;
+  size_t hist, chunk_base, offsets, tiles, n_tiles, groups, n_groups, work_ctr, perm, a_perm, h, total;
 };
 
 WsLayout ws_layout(const eb_model_desc& d, const StepShape& s, const eb_step_views* v) {
@@ -84,6 +84,7 @@ WsLayout ws_layout(const eb_model_desc& d, const StepShape& s, const eb_step_vie
   w.n_tiles = take(sizeof(int32_t));
   w.groups = take(sizeof(int4) * (size_t)d.L * (d.E + d.S));
   w.n_groups = take(sizeof(int32_t));
+  w.work_ctr = take(sizeof(int32_t) * kWorkCounters);
   w.perm = (v && v->perm) ? 0 : take(sizeof(int32_t) * (size_t)s.P);
   w.a_perm = (v && v->a_perm) ? 0 : take(eb * (size_t)s.P * d.H);
   w.h = (v && v->h) ? 0 : take(eb * (size_t)s.P * d.F);
@@ -283,6 +284,7 @@ int easybalance_moe_step(const eb_model_desc* desc, int32_t n_run, const eb_work
   int32_t* n_tiles = reinterpret_cast<int32_t*>(base + L.n_tiles);
   int4* groups = reinterpret_cast<int4*>(base + L.groups);
   int32_t* n_groups = reinterpret_cast<int32_t*>(base + L.n_groups);
+  int32_t* work_ctr = reinterpret_cast<int32_t*>(base + L.work_ctr);
   int32_t* perm = (views && views->perm) ? views->perm : reinterpret_cast<int32_t*>(base + L.perm);
   void* a_perm = (views && views->a_perm) ? views->a_perm : base + L.a_perm;
   void* h = (views && views->h) ? views->h : base + L.h;
@@ -292,7 +294,7 @@ int easybalance_moe_step(const eb_model_desc* desc, int32_t n_run, const eb_work
   const int eb = d.dtype == EB_DTYPE_BF16 ? 2 : 4;
   if ((rc = hip_status(launch_perm_count(rt, sh.n_chunks, hist, s), "perm_count"))) return rc;
   if ((rc = hip_status(launch_perm_scan(rt, sh.n_chunks, hist, chunk_base, offsets, tiles, n_tiles,
-                                        groups, n_groups, gemm_bm(d.dtype), sh.max_tiles, s),
+                                        groups, n_groups, gemm_bm(d.dtype), sh.max_tiles, work_ctr, s),
                        "perm_scan")))
     return rc;
   if ((rc = hip_status(launch_perm_scatter(rt, sh.n_chunks, (int)sh.P, eb, chunk_base, perm, inv_out, a_perm, s),
@@ -310,7 +312,9 @@ int easybalance_moe_step(const eb_model_desc* desc, int32_t n_run, const eb_work
   gp.groups = groups;
   gp.n_groups = n_groups;
   gp.max_tiles = sh.max_tiles;
+  gp.work_ctr = work_ctr;
   if ((rc = hip_status(launch_gateup(d.dtype, gp, wt, a_perm, h, s), "gate/up GEMM"))) return rc;
+  gp.work_ctr = work_ctr + kWorkCounters / 2;
   return hip_status(launch_down(d.dtype, gp, wt, h, o_out, s), "down GEMM");
 }
 

@@ -41,7 +41,10 @@ struct GroupedProblem {
   const int4* groups;                      // [n_groups] (key, first row, rows, first row block)
   const int32_t* n_groups;                 // device scalar: non-empty keys
   int32_t max_tiles;                       // grid bound
+  int32_t* work_ctr;                       // [8] per-XCD work counters of this launch, zeroed
 };
+
+constexpr int kWorkCounters = 16;          // 8 per grouped GEMM launch (gate/up, down)
 
 // Device-side entry lookup: largest rho with base[rho] <= v (bases ascending).
 __device__ __forceinline__ int find_entry(const int32_t* base, int n, int v) {
@@ -62,7 +65,7 @@ hipError_t launch_perm_count(const RunTable& rt, int n_chunks, int32_t* hist, hi
 hipError_t launch_perm_scan(const RunTable& rt, int n_chunks, const int32_t* hist,
                             int32_t* chunk_base, int32_t* offsets, int2* tiles,
                             int32_t* n_tiles, int4* groups, int32_t* n_groups, int bm,
-                            int max_tiles, hipStream_t s);
+                            int max_tiles, int32_t* work_ctr, hipStream_t s);
 hipError_t launch_perm_scatter(const RunTable& rt, int n_chunks, int P, int elem_bytes,
                                const int32_t* chunk_base, int32_t* perm, int32_t* inv,
                                void* a_perm, hipStream_t s);

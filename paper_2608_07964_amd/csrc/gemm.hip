@@ -403,29 +403,54 @@ __device__ __forceinline__ void run_item(const GroupedProblem& p, bf16_t* smem, 
 // Persistent grouped GEMM.  Work item = (group, n-tile, m-tile of 256 rows),
 // enumerated group by group, n-tile-major, m-tile fastest, so consecutive
 // items share the weight tile.  Workgroup b runs on XCD b % 8 (round-robin
-// dispatch); XCD x walks its own contiguous eighth of the items with its
-// workgroups side by side, so items running together on one L2 share weight
-// and activation tiles.  Each item runs in the tile shape of the rows it
-// holds; all shapes accumulate K in the same order, so a row's result does
-// not depend on the shape it was computed in.
+// dispatch) and takes items from its XCD's contiguous eighth of the list
+// through that XCD's atomic counter, so items running together on one L2
+// share weight and activation tiles and no workgroup idles while its XCD has
+// work; once its XCD's range is drained it takes items from the other XCDs'
+// ranges.  Every item is taken exactly once whichever workgroup takes it.
+// The counter increment for the next item is issued at the start of the
+// current one and its result used at its end.  Each item runs in the tile
+// shape of the rows it holds; all shapes accumulate K in the same order, so a
+// row's result does not depend on the shape or on which workgroup ran it.
 template <int MODE>
 __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_bf16(GroupedProblem p, WeightTable wt,
                                                                  const bf16_t* __restrict__ A,
                                                                  bf16_t* __restrict__ C,
                                                                  int n_ntiles) {
   __shared__ __attribute__((aligned(1024))) bf16_t smem[kLdsElems];
+  // the next item index is broadcast through the first word of the ring,
+  // which no load writes between an item's last K stage and the next prologue
+  int* s_next = reinterpret_cast<int*>(smem);
   // the LDS ring is written by global->LDS loads the compiler does not see
   asm volatile("" ::"v"(smem) : "memory");
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int xcd = blockIdx.x % kXcds, slot = blockIdx.x / kXcds, nslots = gridDim.x / kXcds;
+  const int xcd = blockIdx.x % kXcds;
   const int G = *p.n_groups;
   const long long total = (long long)(*p.n_tiles) * n_ntiles;
-  const int lo = (int)((xcd * total) / kXcds), hi = (int)(((xcd + 1) * total) / kXcds);
+  auto range_lo = [&](int x) { return (int)((x * total) / kXcds); };
   const int K = MODE == MODE_GATEUP ? p.H : p.F;
   const int ES = p.E + p.S;
 
-  for (int it = lo + slot; it < hi; it += nslots) {
+  // thread 0: the XCD whose range it draws from, and the first item
+  int victim = xcd;
+  auto settle = [&](int got) {  // item index from a counter value of victim's range, or -1
+    int it = range_lo(victim) + got;
+    while (it >= range_lo(victim + 1)) {
+      victim = victim + 1 == kXcds ? 0 : victim + 1;
+      if (victim == xcd) return -1;
+      it = range_lo(victim) + atomicAdd(&p.work_ctr[victim], 1);
+    }
+    return it;
+  };
+  if (tid == 0) *s_next = settle(atomicAdd(&p.work_ctr[victim], 1));
+  __syncthreads();
+  int it = *s_next;
+  __syncthreads();
+
+  while (it >= 0) {
+    int got = 0;
+    if (tid == 0) got = atomicAdd(&p.work_ctr[victim], 1);
     // group of this item: the last g with cum_mt[g] * n_ntiles <= it
     int glo = 0, ghi = G - 1;
     while (glo < ghi) {
@@ -448,8 +473,13 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_bf16(GroupedProblem 
       run_item<CfgMid, MODE>(p, smem, A, C, Bbase, row0, row_end, ni, K, wave, lane);
     else
       run_item<CfgSkinny, MODE>(p, smem, A, C, Bbase, row0, row_end, ni, K, wave, lane);
+    if (tid == 0) *s_next = settle(got);
+    __syncthreads();
+    it = *s_next;
+    __syncthreads();  // every thread has read it before the next prologue refills the ring
   }
 }
+
 // ---------------------------------------------------------------------------
 // fp32 path
 constexpr int FBM = 64, FBN = 64, FBK = 16;

@@ -8,7 +8,8 @@
 //   perm_scan_kernel     one workgroup: per-key totals, offsets, per-chunk bases,
 //                        the GEMM tile list (key, first row) of BM-row blocks and
 //                        the list of non-empty groups (key, first row, rows,
-//                        index of its first row block)
+//                        index of its first row block); it also clears the
+//                        work counters of the step's grouped GEMM launches
 //   perm_scatter_kernel  per chunk: stable rank of each pair inside its key from
 //                        per-wavefront 64-bit expert masks (popcount of the lanes
 //                        below), then inv and perm
@@ -64,8 +65,10 @@ __device__ int block_exclusive_scan(int v, int* sm, int* total) {
 __global__ __launch_bounds__(kScanThreads) void perm_scan_kernel(
     RunTable rt, int n_chunks, const int32_t* __restrict__ hist, int32_t* __restrict__ chunk_base,
     int32_t* __restrict__ offsets, int2* __restrict__ tiles, int32_t* __restrict__ n_tiles,
-    int4* __restrict__ groups, int32_t* __restrict__ n_groups, int bm, int max_tiles) {
+    int4* __restrict__ groups, int32_t* __restrict__ n_groups, int bm, int max_tiles,
+    int32_t* __restrict__ work_ctr) {
   extern __shared__ int smem[];  // running[n_keys] | scan[kScanThreads]
+  if (threadIdx.x < kWorkCounters) work_ctr[threadIdx.x] = 0;
   const int ES = rt.E + rt.S;
   const int n_keys = rt.L * ES;
   int* running = smem;
@@ -209,11 +212,12 @@ hipError_t launch_perm_count(const RunTable& rt, int n_chunks, int32_t* hist, hi
 hipError_t launch_perm_scan(const RunTable& rt, int n_chunks, const int32_t* hist,
                             int32_t* chunk_base, int32_t* offsets, int2* tiles,
                             int32_t* n_tiles, int4* groups, int32_t* n_groups, int bm,
-                            int max_tiles, hipStream_t s) {
+                            int max_tiles, int32_t* work_ctr, hipStream_t s) {
   const size_t smem = sizeof(int) * ((size_t)rt.L * (rt.E + rt.S) + kScanThreads);
   prof_start(EB_K_PERM_SCAN, s);
   hipLaunchKernelGGL(perm_scan_kernel, dim3(1), dim3(kScanThreads), smem, s, rt, n_chunks, hist,
-                     chunk_base, offsets, tiles, n_tiles, groups, n_groups, bm, max_tiles);
+                     chunk_base, offsets, tiles, n_tiles, groups, n_groups, bm, max_tiles,
+                     work_ctr);
   prof_stop(EB_K_PERM_SCAN, s);
   return hipGetLastError();
 }
