@@ -65,7 +65,8 @@ StepShape step_shape(const eb_model_desc& d, int n_run, const int32_t* T) {
 }
 
 struct WsLayout {
-  size_t hist, chunk_base, offsets, tiles, n_tiles, groups, n_groups, work_ctr, perm, a_perm, h, total;
+  size_t hist, chunk_base, offsets, tiles, n_tiles, groups, n_groups, work_ctr, partial, perm, a_perm,
+      h, total;
 };
 
 WsLayout ws_layout(const eb_model_desc& d, const StepShape& s, const eb_step_views* v) {
@@ -85,6 +86,7 @@ WsLayout ws_layout(const eb_model_desc& d, const StepShape& s, const eb_step_vie
   w.groups = take(sizeof(int4) * (size_t)d.L * (d.E + d.S));
   w.n_groups = take(sizeof(int32_t));
   w.work_ctr = take(sizeof(int32_t) * kWorkCounters);
+  w.partial = down_ksplit(d.dtype, d.F) > 1 ? take(sizeof(float) * 2 * (size_t)s.P * d.H) : 0;
   w.perm = (v && v->perm) ? 0 : take(sizeof(int32_t) * (size_t)s.P);
   w.a_perm = (v && v->a_perm) ? 0 : take(eb * (size_t)s.P * d.H);
   w.h = (v && v->h) ? 0 : take(eb * (size_t)s.P * d.F);
@@ -285,6 +287,7 @@ int easybalance_moe_step(const eb_model_desc* desc, int32_t n_run, const eb_work
   int4* groups = reinterpret_cast<int4*>(base + L.groups);
   int32_t* n_groups = reinterpret_cast<int32_t*>(base + L.n_groups);
   int32_t* work_ctr = reinterpret_cast<int32_t*>(base + L.work_ctr);
+  float* partial = L.partial ? reinterpret_cast<float*>(base + L.partial) : nullptr;
   int32_t* perm = (views && views->perm) ? views->perm : reinterpret_cast<int32_t*>(base + L.perm);
   void* a_perm = (views && views->a_perm) ? views->a_perm : base + L.a_perm;
   void* h = (views && views->h) ? views->h : base + L.h;
@@ -313,8 +316,12 @@ int easybalance_moe_step(const eb_model_desc* desc, int32_t n_run, const eb_work
   gp.n_groups = n_groups;
   gp.max_tiles = sh.max_tiles;
   gp.work_ctr = work_ctr;
+  gp.ksplit = 1;
+  gp.partial = nullptr;
   if ((rc = hip_status(launch_gateup(d.dtype, gp, wt, a_perm, h, s), "gate/up GEMM"))) return rc;
   gp.work_ctr = work_ctr + kWorkCounters / 2;
+  gp.ksplit = down_ksplit(d.dtype, d.F);
+  gp.partial = partial;
   return hip_status(launch_down(d.dtype, gp, wt, h, o_out, s), "down GEMM");
 }
 

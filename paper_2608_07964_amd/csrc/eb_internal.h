@@ -42,7 +42,13 @@ struct GroupedProblem {
   const int32_t* n_groups;                 // device scalar: non-empty keys
   int32_t max_tiles;                       // grid bound
   int32_t* work_ctr;                       // [8] per-XCD work counters of this launch, zeroed
+  int32_t ksplit;                          // 1, or 2: K halves computed by separate items
+  float* partial;                          // ksplit 2: [2][P][N] fp32 partial sums
 };
+
+// K split of the down GEMM: two halves for long K (a rule on the shape only,
+// so every schedule computes a row the same way).
+inline int down_ksplit(int dtype, int F) { return dtype == EB_DTYPE_BF16 && F >= 8192 ? 2 : 1; }
 
 constexpr int kWorkCounters = 16;          // 8 per grouped GEMM launch (gate/up, down)
 

@@ -296,22 +296,26 @@ __device__ __forceinline__ void k_loop(const KLoop& L, floatx16 (&acc)[C::MB][C:
   }
 }
 
-// One work item (m-tile row0.. of group rows ending at row_end, n-tile ni)
-// in tile shape C.
+// One work item (m-tile row0.. of group rows ending at row_end, n-tile ni,
+// K stages ks0 .. ks0+nks-1) in tile shape C.  part == nullptr: the item
+// covers all of K and writes the output; else it writes its fp32 partial
+// sums to part (row-major, N = H columns).
 template <class C, int MODE>
 __device__ __forceinline__ void run_item(const GroupedProblem& p, bf16_t* smem, const bf16_t* A,
                                          bf16_t* C_out, const bf16_t* Bbase, int row0, int row_end,
-                                         int ni, int K, int wave, int lane) {
+                                         int ni, int K, int ks0, int nks, float* part, int wave,
+                                         int lane) {
   const int wm = wave / C::WN, wn = wave % C::WN;
   const int lrow = lane & 31, khalf = lane >> 5;
   const int lr = lane >> 3, lp = lane & 7;
-  const bf16_t* Atile = A + (size_t)row0 * K;
+  const int k_off = ks0 * BK;  // first K column of the item
+  const bf16_t* Atile = A + (size_t)row0 * K + k_off;
   const int a_rows = min(C::BM, p.P - row0);  // rows past it read zeros; their results are discarded
 
   KLoop kl;
   kl.smem = smem;
-  kl.ra = buffer_rsrc(Atile, (uint32_t)(a_rows * K * 2));
-  kl.rb = buffer_rsrc(Bbase, (uint32_t)((MODE == MODE_GATEUP ? 2 * p.F : p.H) * K * 2));
+  kl.ra = buffer_rsrc(Atile, (uint32_t)(a_rows * K * 2 - k_off * 2));
+  kl.rb = buffer_rsrc(Bbase + k_off, (uint32_t)((MODE == MODE_GATEUP ? 2 * p.F : p.H) * K * 2 - k_off * 2));
   kl.row_bytes = K * 2;
   {
     // swizzle of the wave's first load row of each operand; odd j flips bit 2
@@ -342,7 +346,7 @@ __device__ __forceinline__ void run_item(const GroupedProblem& p, bf16_t* smem, 
   kl.lds_a = (wm * C::TM + lrow) * BK;
   kl.lds_b = (wn * C::TN + lrow) * BK;
   kl.sw = (lrow >> 1) & 7;
-  kl.nk = K / BK;
+  kl.nk = nks;
   kl.khalf = khalf;
 
   floatx16 acc[C::MB][C::NB];
@@ -389,6 +393,12 @@ __device__ __forceinline__ void run_item(const GroupedProblem& p, bf16_t* smem, 
           const int f = ni * (BN / 2) + wn * (C::TN / 2) + nb * 32 + lrow;
           C_out[(size_t)row * p.F + f] = f32_to_bf16(swiglu(acc[mb][nb][v], acc[mb][nb + C::NB / 2][v]));
         }
+      } else if (part != nullptr) {
+#pragma unroll
+        for (int nb = 0; nb < C::NB; ++nb) {
+          const int n = ni * BN + wn * C::TN + nb * 32 + lrow;
+          part[(size_t)row * p.H + n] = acc[mb][nb][v];
+        }
       } else {
 #pragma unroll
         for (int nb = 0; nb < C::NB; ++nb) {
@@ -427,7 +437,9 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_bf16(GroupedProblem 
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int xcd = blockIdx.x % kXcds;
   const int G = *p.n_groups;
-  const long long total = (long long)(*p.n_tiles) * n_ntiles;
+  const int ksplit = MODE == MODE_DOWN ? p.ksplit : 1;
+  const int nsub = n_ntiles * ksplit;  // items per m-tile
+  const long long total = (long long)(*p.n_tiles) * nsub;
   auto range_lo = [&](int x) { return (int)((x * total) / kXcds); };
   const int K = MODE == MODE_GATEUP ? p.H : p.F;
   const int ES = p.E + p.S;
@@ -451,16 +463,21 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_bf16(GroupedProblem 
   while (it >= 0) {
     int got = 0;
     if (tid == 0) got = atomicAdd(&p.work_ctr[victim], 1);
-    // group of this item: the last g with cum_mt[g] * n_ntiles <= it
+    // group of this item: the last g with cum_mt[g] * nsub <= it
     int glo = 0, ghi = G - 1;
     while (glo < ghi) {
       const int mid = (glo + ghi + 1) >> 1;
-      if ((long long)p.groups[mid].w * n_ntiles <= it) glo = mid; else ghi = mid - 1;
+      if ((long long)p.groups[mid].w * nsub <= it) glo = mid; else ghi = mid - 1;
     }
     const int4 gd = p.groups[glo];  // key, first row, rows, first m-tile
     const int mt = (gd.z + BM - 1) / BM;
-    const int local = it - gd.w * n_ntiles;
-    const int ni = local / mt, mi = local - ni * mt;
+    // within the group: K part slowest, then n-tile, m-tile fastest
+    const int local = it - gd.w * nsub;
+    const int kh = local / (mt * n_ntiles);
+    const int rem = local - kh * mt * n_ntiles;
+    const int ni = rem / mt, mi = rem - ni * mt;
+    const int nks = K / BK / ksplit, ks0 = kh * nks;
+    float* part = ksplit > 1 ? p.partial + (size_t)kh * p.P * p.H : nullptr;
     const int row0 = gd.y + mi * BM, row_end = gd.y + gd.z;
     const int layer = gd.x / ES, e = gd.x - layer * ES;
     const bf16_t* Bbase = MODE == MODE_GATEUP
@@ -468,11 +485,11 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_bf16(GroupedProblem 
         : static_cast<const bf16_t*>(wt.dn[layer]) + (size_t)e * p.H * p.F;
     const int rows = row_end - row0;
     if (rows > CfgMid::BM)
-      run_item<CfgBig, MODE>(p, smem, A, C, Bbase, row0, row_end, ni, K, wave, lane);
+      run_item<CfgBig, MODE>(p, smem, A, C, Bbase, row0, row_end, ni, K, ks0, nks, part, wave, lane);
     else if (rows > CfgSkinny::BM)
-      run_item<CfgMid, MODE>(p, smem, A, C, Bbase, row0, row_end, ni, K, wave, lane);
+      run_item<CfgMid, MODE>(p, smem, A, C, Bbase, row0, row_end, ni, K, ks0, nks, part, wave, lane);
     else
-      run_item<CfgSkinny, MODE>(p, smem, A, C, Bbase, row0, row_end, ni, K, wave, lane);
+      run_item<CfgSkinny, MODE>(p, smem, A, C, Bbase, row0, row_end, ni, K, ks0, nks, part, wave, lane);
     if (tid == 0) *s_next = settle(got);
     __syncthreads();
     it = *s_next;
@@ -550,6 +567,20 @@ __global__ __launch_bounds__(256) void grouped_gemm_f32(GroupedProblem p, Weight
   }
 }
 
+// o = dtype(p0 + p1) for the K halves of a split down GEMM, 4 elements per
+// thread (n = P*H is a multiple of 256).
+__global__ __launch_bounds__(256) void split_sum_kernel(const float* __restrict__ part, long long n,
+                                                        bf16_t* __restrict__ o) {
+  const long long i = ((long long)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (i >= n) return;
+  const float4 a = *reinterpret_cast<const float4*>(part + i);
+  const float4 b = *reinterpret_cast<const float4*>(part + n + i);
+  uint2 u;
+  u.x = (uint32_t)f32_to_bf16(a.x + b.x) | ((uint32_t)f32_to_bf16(a.y + b.y) << 16);
+  u.y = (uint32_t)f32_to_bf16(a.z + b.z) | ((uint32_t)f32_to_bf16(a.w + b.w) << 16);
+  *reinterpret_cast<uint2*>(o + i) = u;
+}
+
 }  // namespace
 
 int gemm_bm(int dtype) { return dtype == EB_DTYPE_BF16 ? BM : FBM; }
@@ -587,6 +618,11 @@ hipError_t launch_down(int dtype, const GroupedProblem& p, const WeightTable& wt
   if (dtype == EB_DTYPE_BF16) {
     hipLaunchKernelGGL(grouped_gemm_bf16<MODE_DOWN>, dim3(persistent_grid()), dim3(kThreads), 0, s,
                        p, wt, static_cast<const bf16_t*>(h), static_cast<bf16_t*>(o), p.H / BN);
+    if (p.ksplit > 1) {
+      const long long n = (long long)p.P * p.H;
+      hipLaunchKernelGGL(split_sum_kernel, dim3((unsigned)((n / 4 + 255) / 256)), dim3(256), 0, s,
+                         p.partial, n, static_cast<bf16_t*>(o));
+    }
   } else {
     hipLaunchKernelGGL(grouped_gemm_f32<MODE_DOWN>, dim3(p.max_tiles, p.H / FBN), dim3(256), 0, s,
                        p, wt, static_cast<const float*>(h), static_cast<float*>(o));

@@ -25,6 +25,10 @@ pytestmark = pytest.mark.gpu
 
 MINIS = [CONFIGS[0]] + [mini(c) for c in CONFIGS[1:]]
 IDS = [c.name for c in MINIS]
+# long K (F >= 8192): the down GEMM runs its two K halves as separate items
+LONGK = mini(CONFIGS[1], H=256, F=8192, T=96, L=2)
+STEP_CFGS = MINIS + [LONGK]
+STEP_IDS = IDS + [LONGK.name + "_longk"]
 
 
 def _binding():
@@ -87,7 +91,7 @@ def _route_entry(B, desc, cfg, inp, j, l, T, device):
     return bufs
 
 
-@pytest.mark.parametrize("cfg", MINIS, ids=IDS)
+@pytest.mark.parametrize("cfg", STEP_CFGS, ids=STEP_IDS)
 def test_moe_step_and_combine_stage(cfg, device):
     """One cross-layer step with entries at different layers, ragged and empty
     token counts; every stage checked against the oracle on the GPU's inputs."""
@@ -182,7 +186,7 @@ def test_tiny_fp32_end_to_end_free_running(device):
     assert_close(to_np(st.x), ref.x[cfg.L], cfg.dtype, "x final")
 
 
-@pytest.mark.parametrize("cfg", MINIS, ids=IDS)
+@pytest.mark.parametrize("cfg", STEP_CFGS, ids=STEP_IDS)
 def test_schedule_invariance_and_replay(cfg, device):
     """Cross-layer joint execution is lossless (Section 4.1): the EB schedule
     and the per-layer lock-step schedule give bit-identical hidden states, and
