@@ -55,6 +55,7 @@ constexpr int kWaves = 8;                        // two wavefronts per SIMD
 constexpr int kThreads = 64 * kWaves;
 constexpr int kKsteps = BK / 16;                 // MFMA k-steps per stage
 constexpr int kBLoads = BN / (8 * kWaves);       // 8-row B blocks per wave per stage
+static_assert(kBLoads == BK / 16, "one B load per k-step");
 constexpr int kXcds = 8;
 
 template <int BM_, int WM_, int SA_, int SB_>
@@ -162,20 +163,24 @@ __device__ __forceinline__ void issue_a(const KLoop& L, int s, int slot) {
                                              (L.a_row0 + 8 * j) * L.row_bytes + ko, 0, 0);
 }
 template <class C>
-__device__ __forceinline__ void issue_b(const KLoop& L, int s, int slot) {
+__device__ __forceinline__ void issue_b_part(const KLoop& L, int s, int slot, int j) {
   bf16_t* d = L.smem + C::B_RING + slot * C::B_ELEMS + L.lds_b_load;
-  const int ko = s * BK * 2;
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(L.rb, d + j * 8 * BK, 16, L.b_lane[j & 1],
+                                           L.b_row[j] * L.row_bytes + s * BK * 2, 0, 0);
+}
+template <class C>
+__device__ __forceinline__ void issue_b(const KLoop& L, int s, int slot) {
 #pragma unroll
-  for (int j = 0; j < kBLoads; ++j)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(L.rb, d + j * 8 * BK, 16, L.b_lane[j & 1],
-                                             L.b_row[j] * L.row_bytes + ko, 0, 0);
+  for (int j = 0; j < kBLoads; ++j) issue_b_part<C>(L, s, slot, j);
 }
 
 // Load order: the prologue issues A(s) (s < SA) and B(s) (s < SB) for
-// s = 0, 1, ..., A before B; step kt issues A(kt+SA) then B(kt+SB) (stages
-// < nk only).  Loads complete in issue order, so "A(t) and B(t) have landed"
-// is "at most n loads are in flight", n = the loads issued after the later of
-// the two.
+// s = 0, 1, ..., A before B; step kt issues A(kt+SA), then the first of the
+// kBLoads loads of B(kt+SB), and one more of them before each of the first
+// three k-steps of step kt+1 (stages < nk only), so no wave issues a burst of
+// loads at once.  Loads complete in issue order, so "A(t) and B(t) have
+// landed" is "at most n loads are in flight", n = the loads issued after the
+// later of the two (every load of B(t) is issued before step t-1 waits).
 template <class C>
 __device__ __forceinline__ int loads_after_stage0(int nk) {
   int n = 0;
@@ -267,9 +272,11 @@ __device__ __forceinline__ void k_loop(const KLoop& L, floatx16 (&acc)[C::MB][C:
   Frags<C> f[2];
   if (NACT > 0) read_frags<C, NACT>(L, 0, 0, 0, f[0]);
   int ca = 0, cb = 0;  // slots of stage kt
+  int pb_s = -1, pb_slot = 0;  // B stage whose remaining loads are still to issue
   for (int kt = 0; kt < nk; ++kt) {
 #pragma unroll
     for (int ks = 0; ks < kKsteps - 1; ++ks) {
+      if (pb_s >= 0) issue_b_part<C>(L, pb_s, pb_slot, ks + 1);
       if (NACT > 0) {
         read_frags<C, NACT>(L, ca, cb, ks + 1, f[(ks + 1) & 1]);
         mfmas<C, NACT>(f[ks & 1], acc);
@@ -284,7 +291,12 @@ __device__ __forceinline__ void k_loop(const KLoop& L, floatx16 (&acc)[C::MB][C:
     wait_le(loads_after_next<C>(kt, nk));
     bar();
     if (kt + C::SA < nk) issue_a<C>(L, kt + C::SA, ca);
-    if (kt + C::SB < nk) issue_b<C>(L, kt + C::SB, cb);
+    pb_s = -1;
+    if (kt + C::SB < nk) {
+      issue_b_part<C>(L, kt + C::SB, cb, 0);
+      pb_s = kt + C::SB;
+      pb_slot = cb;
+    }
     const int na = ca + 1 == C::SA ? 0 : ca + 1;
     const int nb = cb + 1 == C::SB ? 0 : cb + 1;
     if (NACT > 0) {
