@@ -55,7 +55,8 @@ constexpr int kWaves = 8;                        // two wavefronts per SIMD
 constexpr int kThreads = 64 * kWaves;
 constexpr int kKsteps = BK / 16;                 // MFMA k-steps per stage
 constexpr int kBLoads = BN / (8 * kWaves);       // 8-row B blocks per wave per stage
-static_assert(kBLoads == BK / 16, "one B load per k-step");
+constexpr int kBPart = kBLoads / (BK / 16);      // B loads issued per k-step
+static_assert(kBPart * (BK / 16) == kBLoads, "B loads split evenly over the k-steps");
 constexpr int kXcds = 8;
 
 template <int BM_, int WM_, int SA_, int SB_>
@@ -162,21 +163,26 @@ __device__ __forceinline__ void issue_a(const KLoop& L, int s, int slot) {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(L.ra, d + j * 8 * BK, 16, L.a_lane[j & 1],
                                              (L.a_row0 + 8 * j) * L.row_bytes + ko, 0, 0);
 }
+// Part q (q < BK/16) of the B loads of stage s: loads j = q*kBPart .. +kBPart-1.
 template <class C>
-__device__ __forceinline__ void issue_b_part(const KLoop& L, int s, int slot, int j) {
+__device__ __forceinline__ void issue_b_part(const KLoop& L, int s, int slot, int q) {
   bf16_t* d = L.smem + C::B_RING + slot * C::B_ELEMS + L.lds_b_load;
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(L.rb, d + j * 8 * BK, 16, L.b_lane[j & 1],
-                                           L.b_row[j] * L.row_bytes + s * BK * 2, 0, 0);
+#pragma unroll
+  for (int i = 0; i < kBPart; ++i) {
+    const int j = q * kBPart + i;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(L.rb, d + j * 8 * BK, 16, L.b_lane[j & 1],
+                                             L.b_row[j] * L.row_bytes + s * BK * 2, 0, 0);
+  }
 }
 template <class C>
 __device__ __forceinline__ void issue_b(const KLoop& L, int s, int slot) {
 #pragma unroll
-  for (int j = 0; j < kBLoads; ++j) issue_b_part<C>(L, s, slot, j);
+  for (int q = 0; q < BK / 16; ++q) issue_b_part<C>(L, s, slot, q);
 }
 
 // Load order: the prologue issues A(s) (s < SA) and B(s) (s < SB) for
-// s = 0, 1, ..., A before B; step kt issues A(kt+SA), then the first of the
-// kBLoads loads of B(kt+SB), and one more of them before each of the first
+// s = 0, 1, ..., A before B; step kt issues A(kt+SA), then the first quarter
+// of the loads of B(kt+SB), and one more quarter before each of the first
 // three k-steps of step kt+1 (stages < nk only), so no wave issues a burst of
 // loads at once.  Loads complete in issue order, so "A(t) and B(t) have
 // landed" is "at most n loads are in flight", n = the loads issued after the
