@@ -2,7 +2,8 @@
 // For every token of every micro-batch in the step (Eq. 1 plus the residual
 // of Section 2.1):
 //   x[t] += sum_{r<k} w[t][r] * o[inv[q(t,r)]] + sum_{s<S} o[inv[q(t,k+s)]]
-// One wavefront per token, 4 consecutive elements per lane per pass, the sum
+// One workgroup per token; each thread owns 8 consecutive elements per pass
+// of 2048 and issues the loads of all k+S rows of a pass at once.  The sum is
 // formed in fp32 in slot order (routed ascending, then shared) before the
 // residual add, so each token's result is independent of the schedule.
 #include "eb_internal.h"
@@ -11,59 +12,74 @@
 namespace eb {
 namespace {
 
+constexpr int kCombThreads = 256;
+
+// 8 consecutive elements of an o row, as fp32.
 template <typename TO>
-struct Load4;
+struct Row8;
 template <>
-struct Load4<float> {
-  __device__ static __forceinline__ float4 at(const float* p) {
-    return *reinterpret_cast<const float4*>(p);
+struct Row8<float> {
+  float4 a, b;
+  __device__ __forceinline__ void load(const float* p) {
+    a = reinterpret_cast<const float4*>(p)[0];
+    b = reinterpret_cast<const float4*>(p)[1];
+  }
+  __device__ __forceinline__ float at(int i) const {
+    const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+    return v[i];
   }
 };
 template <>
-struct Load4<bf16_t> {
-  __device__ static __forceinline__ float4 at(const bf16_t* p) {
-    const uint2 u = *reinterpret_cast<const uint2*>(p);
-    return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
-                       __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
+struct Row8<bf16_t> {
+  uint4 u;
+  __device__ __forceinline__ void load(const bf16_t* p) { u = *reinterpret_cast<const uint4*>(p); }
+  __device__ __forceinline__ float at(int i) const {
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+    const uint32_t x = w[i >> 1];
+    return __uint_as_float((i & 1) ? (x & 0xffff0000u) : (x << 16));
   }
 };
 
 template <typename TO>
-__global__ __launch_bounds__(256) void combine_kernel(RunTable rt, int total, const TO* __restrict__ o,
-                                                      const int32_t* __restrict__ inv) {
-  const int lane = threadIdx.x & 63;
-  const int g = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (g >= total) return;
+__global__ __launch_bounds__(kCombThreads) void combine_kernel(RunTable rt, int total,
+                                                               const TO* __restrict__ o,
+                                                               const int32_t* __restrict__ inv) {
+  __shared__ int s_row[kMaxSlots];
+  __shared__ float s_w[kMaxSlots];
+  const int g = blockIdx.x;
   const int rho = find_entry(rt.tok_base, rt.n, g);
   const int t = g - rt.tok_base[rho];
   const int k = rt.k, slots = rt.k + rt.S, H = rt.H;
-  const size_t q0 = (size_t)g * slots;
   const int P = total * slots;  // grouped rows; inv is clamped into [0, P)
+  if (threadIdx.x < slots) {
+    s_row[threadIdx.x] = min(max(inv[(size_t)g * slots + threadIdx.x], 0), P - 1);
+    s_w[threadIdx.x] = threadIdx.x < k ? rt.w[rho][(size_t)t * k + threadIdx.x] : 1.f;
+  }
+  __syncthreads();
   float* x = rt.x[rho] + (size_t)t * H;
-  const float* w = rt.w[rho] + (size_t)t * k;
-  for (int c = lane * 4; c < H; c += 256) {
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int r = 0; r < k; ++r) {
-      const float wr = w[r];
-      const float4 v = Load4<TO>::at(o + (size_t)min(max(inv[q0 + r], 0), P - 1) * H + c);
-      acc.x = fmaf(wr, v.x, acc.x);
-      acc.y = fmaf(wr, v.y, acc.y);
-      acc.z = fmaf(wr, v.z, acc.z);
-      acc.w = fmaf(wr, v.w, acc.w);
+  for (int c = threadIdx.x * 8; c < H; c += kCombThreads * 8) {
+    Row8<TO> v[kMaxSlots];
+#pragma unroll
+    for (int r = 0; r < kMaxSlots; ++r)
+      if (r < slots) v[r].load(o + (size_t)s_row[r] * H + c);
+    float4 x0 = reinterpret_cast<float4*>(x + c)[0];
+    float4 x1 = reinterpret_cast<float4*>(x + c)[1];
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int r = 0; r < kMaxSlots; ++r) {
+      if (r < k) {
+        const float wr = s_w[r];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[i] = fmaf(wr, v[r].at(i), acc[i]);
+      } else if (r < slots) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[i] += v[r].at(i);
+      }
     }
-    for (int r = k; r < slots; ++r) {
-      const float4 v = Load4<TO>::at(o + (size_t)min(max(inv[q0 + r], 0), P - 1) * H + c);
-      acc.x += v.x;
-      acc.y += v.y;
-      acc.z += v.z;
-      acc.w += v.w;
-    }
-    float4 xv = *reinterpret_cast<float4*>(x + c);
-    xv.x += acc.x;
-    xv.y += acc.y;
-    xv.z += acc.z;
-    xv.w += acc.w;
-    *reinterpret_cast<float4*>(x + c) = xv;
+    x0.x += acc[0]; x0.y += acc[1]; x0.z += acc[2]; x0.w += acc[3];
+    x1.x += acc[4]; x1.y += acc[5]; x1.z += acc[6]; x1.w += acc[7];
+    reinterpret_cast<float4*>(x + c)[0] = x0;
+    reinterpret_cast<float4*>(x + c)[1] = x1;
   }
 }
 
@@ -73,10 +89,10 @@ hipError_t launch_combine(const RunTable& rt, int total_tokens, int dtype, const
                           const int32_t* inv, hipStream_t s) {
   prof_start(EB_K_COMBINE, s);
   if (dtype == EB_DTYPE_BF16)
-    hipLaunchKernelGGL(combine_kernel<bf16_t>, dim3((total_tokens + 3) / 4), dim3(256), 0, s, rt,
+    hipLaunchKernelGGL(combine_kernel<bf16_t>, dim3(total_tokens), dim3(kCombThreads), 0, s, rt,
                        total_tokens, static_cast<const bf16_t*>(o), inv);
   else
-    hipLaunchKernelGGL(combine_kernel<float>, dim3((total_tokens + 3) / 4), dim3(256), 0, s, rt,
+    hipLaunchKernelGGL(combine_kernel<float>, dim3(total_tokens), dim3(kCombThreads), 0, s, rt,
                        total_tokens, static_cast<const float*>(o), inv);
   prof_stop(EB_K_COMBINE, s);
   return hipGetLastError();
