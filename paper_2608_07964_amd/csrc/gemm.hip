@@ -98,20 +98,6 @@ __device__ __forceinline__ void wait_vm() {
 }
 constexpr int kWaitLgkm0 = 15 | (3 << 14) | (7 << 4);
 
-// Wait until at most n of this wave's loads are in flight: the largest rung
-// <= n of a ladder that holds every count the K loops below ask for.
-__device__ __forceinline__ void wait_le(int n) {
-  if (n >= 16) wait_vm<16>();
-  else if (n >= 15) wait_vm<15>();
-  else if (n >= 12) wait_vm<12>();
-  else if (n >= 10) wait_vm<10>();
-  else if (n >= 8) wait_vm<8>();
-  else if (n >= 6) wait_vm<6>();
-  else if (n >= 5) wait_vm<5>();
-  else if (n >= 4) wait_vm<4>();
-  else wait_vm<0>();
-}
-
 // Bare workgroup barrier: this wave's outstanding buffer->LDS loads stay in
 // flight across it (a fenced __syncthreads would drain them).
 __device__ __forceinline__ void bar() {
@@ -180,44 +166,45 @@ __device__ __forceinline__ void issue_b(const KLoop& L, int s, int slot) {
   for (int q = 0; q < BK / 16; ++q) issue_b_part<C>(L, s, slot, q);
 }
 
-// Load order: the prologue issues A(s) (s < SA) and B(s) (s < SB) for
-// s = 0, 1, ..., A before B; step kt issues A(kt+SA), then the first quarter
-// of the loads of B(kt+SB), and one more quarter before each of the first
-// three k-steps of step kt+1 (stages < nk only), so no wave issues a burst of
-// loads at once.  Loads complete in issue order, so "A(t) and B(t) have
-// landed" is "at most n loads are in flight", n = the loads issued after the
-// later of the two (every load of B(t) is issued before step t-1 waits).
+// Load order.  Stage t's A loads and the first quarter of its B loads are
+// issued right after the barrier of step t-SA resp. t-SB, A first; the other
+// three quarters of B(t) go out before the first three k-steps of the step
+// after that, one quarter each, so no wave issues a burst of loads at once.
+// The prologue issues stages 0 .. SB-1 in the same order as if the steps
+// -SB .. -1 had run (the last three quarters of B(SB-1) go out in step 0).
+// Every load is issued, also for stages past the item's last one: those load
+// the last stage again into a slot that is never read, so the number of loads
+// in flight at every wait is a constant.  Loads complete in issue order, so
+// "A(t) and B(t) have landed" is "at most n loads are in flight", n = the
+// loads issued after the later of the two.
 template <class C>
-__device__ __forceinline__ int loads_after_stage0(int nk) {
-  int n = 0;
-#pragma unroll
-  for (int s = 1; s < C::SB; ++s) {
-    if (s < C::SA && s < nk) n += C::A_LOADS;
-    if (s < nk) n += kBLoads;
-  }
-  return n;
-}
-// In step kt, waiting for stage kt+1 (issued loads: prologue and steps < kt).
-template <class C>
-__device__ __forceinline__ int loads_after_next(int kt, int nk) {
-  int n = 0;
-  if (C::SB == C::SA) {
-    // A(t), B(t) are adjacent; after them come stages t+1 .. kt+SA-1
-#pragma unroll
-    for (int s = 2; s < C::SA; ++s)
-      if (kt + s < nk) n += C::A_LOADS + kBLoads;
-  } else {
-    // A(kt+1) is issued after B(kt+1); after it come B(kt+2), then the pairs
-    // A(kt+2..kt+SA-1), B(kt+3..kt+SA)
-    if (kt + 2 < nk) n += kBLoads;
-#pragma unroll
-    for (int s = 2; s < C::SA; ++s) {
-      if (kt + s < nk) n += C::A_LOADS;
-      if (kt + s + 1 < nk) n += kBLoads;
+struct LoadOrder {
+  // loads after the last load of stage 0, when the prologue waits
+  static constexpr int after_stage0() {
+    int n = 0;
+    bool after = false;
+    for (int j = -C::SB; j < 0; ++j) {
+      if (j + C::SA >= 0) {
+        if (after) n += C::A_LOADS;
+        if (j + C::SA == 0 && C::SB == C::SA + 1) after = true;  // A(0) comes after all of B(0)
+      }
+      if (j + C::SB >= 0) {
+        if (after) n += kBPart;
+        if (j + 1 < 0) {
+          if (after) n += kBLoads - kBPart;
+          if (j + C::SB == 0 && C::SB == C::SA) after = true;    // B(0) ends after A(0)
+        }
+      }
     }
+    return n;
   }
-  return n;
-}
+  // loads after the last load of stage kt+1, when step kt waits
+  static constexpr int after_next() {
+    return C::SB == C::SA ? (C::SA - 2) * (C::A_LOADS + kBLoads)
+                          : kBLoads + (C::SA - 2) * (C::A_LOADS + kBLoads);
+  }
+  static_assert(after_next() < 64 && after_stage0() < 64, "vmcnt range");
+};
 
 // Fragment rows of one lane: A rows wm*TM + mb*32 + lrow, B rows
 // wn*TN + nb*32 + lrow; (row >> 1) & 7 = (lrow >> 1) & 7 for all of them, so
@@ -246,14 +233,17 @@ __device__ __forceinline__ void mfmas(const Frags<C>& f, floatx16 (&acc)[C::MB][
       acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[mb], f.b[nb], acc[mb][nb], 0, 0, 0);
 }
 
-// Scheduling groups that spread R fragment reads evenly between M MFMAs.
-template <int R, int M, int I = 0>
-__device__ __forceinline__ void interleave() {
-  if constexpr (I < R) {
-    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one DS read
-    constexpr int q = ((I + 1) * M) / R - (I * M) / R;
-    if constexpr (q > 0) __builtin_amdgcn_sched_group_barrier(0x008, q, 0);  // q MFMAs
-    interleave<R, M, I + 1>();
+// Scheduling groups for one k-step: M MFMAs with R fragment reads and V
+// buffer loads spread evenly between them.
+template <int R, int M, int V, int I = 0>
+__device__ __forceinline__ void interleave3() {
+  if constexpr (I < M) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+    constexpr int r = ((I + 1) * R) / M - (I * R) / M;
+    if constexpr (r > 0) __builtin_amdgcn_sched_group_barrier(0x100, r, 0);  // DS reads
+    constexpr int v = ((I + 1) * V) / M - (I * V) / M;
+    if constexpr (v > 0) __builtin_amdgcn_sched_group_barrier(0x020, v, 0);  // VMEM reads
+    interleave3<R, M, V, I + 1>();
   }
 }
 
@@ -262,56 +252,62 @@ __device__ __forceinline__ void interleave() {
 // the next k-step's fragments read ahead; before the MFMAs of the last k-step
 // the wave waits for its reads of stage kt and its loads of stage kt+1, the
 // barrier publishes stage kt+1 and frees the slots of stage kt, A(kt+SA) and
-// B(kt+SB) are issued into them and the first fragments of stage kt+1 are
-// read.  NACT = active 32-row blocks of the wave's rows (inactive blocks of a
-// ragged tile get neither LDS reads nor MFMAs).
+// B(kt+SB) are issued into them (see the load order above) and the first
+// fragments of stage kt+1 are read.  NACT = active 32-row blocks of the wave's
+// rows (inactive blocks of a ragged tile get neither LDS reads nor MFMAs).
 template <class C, int NACT>
 __device__ __forceinline__ void k_loop(const KLoop& L, floatx16 (&acc)[C::MB][C::NB]) {
-  const int nk = L.nk;
+  const int nk = L.nk, last = nk - 1;
 #pragma unroll
-  for (int s = 0; s < C::SB; ++s) {
-    if (s < C::SA && s < nk) issue_a<C>(L, s, s);
-    if (s < nk) issue_b<C>(L, s, s);
+  for (int j = -C::SB; j < 0; ++j) {
+    if (j + C::SA >= 0) issue_a<C>(L, min(j + C::SA, last), j + C::SA);
+    if (j + C::SB >= 0) {
+      issue_b_part<C>(L, min(j + C::SB, last), j + C::SB, 0);
+      if (j + 1 < 0)
+#pragma unroll
+        for (int q = 1; q < BK / 16; ++q) issue_b_part<C>(L, min(j + C::SB, last), j + C::SB, q);
+    }
   }
-  wait_le(loads_after_stage0<C>(nk));
+  int pb_s = min(C::SB - 1, last), pb_slot = C::SB - 1;  // B stage with quarters still to issue
+  wait_vm<LoadOrder<C>::after_stage0()>();
   bar();
   Frags<C> f[2];
   if (NACT > 0) read_frags<C, NACT>(L, 0, 0, 0, f[0]);
   int ca = 0, cb = 0;  // slots of stage kt
-  int pb_s = -1, pb_slot = 0;  // B stage whose remaining loads are still to issue
   for (int kt = 0; kt < nk; ++kt) {
 #pragma unroll
     for (int ks = 0; ks < kKsteps - 1; ++ks) {
-      if (pb_s >= 0) issue_b_part<C>(L, pb_s, pb_slot, ks + 1);
+      issue_b_part<C>(L, pb_s, pb_slot, ks + 1);
       if (NACT > 0) {
         read_frags<C, NACT>(L, ca, cb, ks + 1, f[(ks + 1) & 1]);
         mfmas<C, NACT>(f[ks & 1], acc);
-        // keep the next k-step's fragment reads spread between this k-step's
-        // MFMAs (the machine scheduler would otherwise move reads next to
-        // their consumers and expose LDS latency)
-        interleave<NACT + C::NB, NACT * C::NB>();
+        // keep the next k-step's fragment reads and the loads spread between
+        // this k-step's MFMAs (the machine scheduler would otherwise move
+        // reads next to their consumers and expose LDS latency)
+        interleave3<NACT + C::NB, NACT * C::NB, kBPart>();
       }
     }
     // every fragment of stage kt is in registers, stage kt+1 has landed
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
-    wait_le(loads_after_next<C>(kt, nk));
+    wait_vm<LoadOrder<C>::after_next()>();
     bar();
-    if (kt + C::SA < nk) issue_a<C>(L, kt + C::SA, ca);
-    pb_s = -1;
-    if (kt + C::SB < nk) {
-      issue_b_part<C>(L, kt + C::SB, cb, 0);
-      pb_s = kt + C::SB;
-      pb_slot = cb;
-    }
+    issue_a<C>(L, min(kt + C::SA, last), ca);
+    pb_s = min(kt + C::SB, last);
+    pb_slot = cb;
+    issue_b_part<C>(L, pb_s, pb_slot, 0);
     const int na = ca + 1 == C::SA ? 0 : ca + 1;
     const int nb = cb + 1 == C::SB ? 0 : cb + 1;
     if (NACT > 0) {
-      if (kt + 1 < nk) read_frags<C, NACT>(L, na, nb, 0, f[0]);
+      read_frags<C, NACT>(L, na, nb, 0, f[0]);
       mfmas<C, NACT>(f[(kKsteps - 1) & 1], acc);
+      interleave3<NACT + C::NB, NACT * C::NB, C::A_LOADS + kBPart>();
     }
     ca = na;
     cb = nb;
   }
+  // the loads of the stages past the last one must land before the next
+  // item's prologue writes the same LDS slots
+  wait_vm<0>();
 }
 
 // One work item (m-tile row0.. of group rows ending at row_end, n-tile ni,
