@@ -52,6 +52,8 @@ extern "C" {
 #define EB_POLICY_MAXUTIL 0
 #define EB_POLICY_CUMUTIL 1
 #define EB_POLICY_DIFFPEAK 2
+#define EB_POLICY_LOCKSTEP 3    /* easybalance_run_pass only: every pooled
+                                   micro-batch every step (per-layer baseline) */
 
 #define EB_MAX_POOL 64          /* micro-batch ids are 0..63 (one bit each)   */
 #define EB_MAXUTIL_MAX_POOL 20  /* MaxUtil enumerates 2^n subsets             */
@@ -223,6 +225,51 @@ int easybalance_moe_step(const eb_model_desc* desc, int32_t n_run, const eb_work
 int easybalance_combine(const eb_model_desc* desc, int32_t n_run, const eb_work* run,
                         float* const* x_inout, const void* o, const int32_t* inv,
                         void* stream);
+
+/*
+ * easybalance_run_pass -- one pass of Algorithm 1 (Section 4.2) for N
+ * micro-batches of T tokens through all L layers, driven by the library:
+ *   route every micro-batch at layer 0 (easybalance_route);
+ *   while the pool S is not empty:
+ *     RunSet = Schedule(S, m) (easybalance_schedule's policies on the pool's
+ *       expert counts, or EB_POLICY_LOCKSTEP: RunSet = S);
+ *     easybalance_moe_step + easybalance_combine on the RunSet, entries in
+ *       ascending micro-batch id, each at its own layer;
+ *     l_j += 1 for j in RunSet; route those with l_j < L; drop the finished.
+ * The results are the ones the same sequence of calls through the other entry
+ * points gives.  The only host<->device synchronisation per step is the copy
+ * of the pool's expert counts to pinned host memory for the scheduler.
+ *
+ * x            device [N][T][H] fp32, updated in place (the residual stream)
+ * gain         device [L][H] fp32;  bias  device [L][E] fp32
+ * Wg           host [L] of device pointers, each [E][H] dtype
+ * W_gu, W_dn   host [L] of device pointers as for easybalance_moe_step
+ * policy, m    EB_POLICY_* and the minimum RunSet size of Algorithm 1
+ *              (MaxUtil: N <= EB_MAXUTIL_MAX_POOL)
+ * state        device scratch of state_bytes >= easybalance_pass_state_size
+ *              (routing outputs, grouped rows, step workspace), 256-byte
+ *              aligned, caller-owned; contents undefined afterwards
+ * max_steps    capacity of the per-step host outputs below
+ * n_steps_out  host out (nullable): steps the pass took (at most N * L)
+ * runsets_out  host out [max_steps] (nullable): RunSet bit masks
+ * layers_out   host out [max_steps][N] (nullable): layer each RunSet member
+ *              ran at, -1 for micro-batches not in the RunSet
+ * step_load_out host out [max_steps][D] (nullable): combined workload W
+ * groups_out   host out [max_steps] (nullable): (layer, expert slot) groups
+ *              with rows in the step (routed experts with a token, plus the
+ *              S shared experts of every layer in the RunSet)
+ * layer_loads_out host out [N][L][D] (nullable): per-device load of each
+ *              micro-batch at each layer, as its routing produced it
+ * Steps past max_steps are run but not recorded.
+ */
+int easybalance_pass_state_size(const eb_model_desc* desc, int32_t N, int32_t T, size_t* bytes);
+int easybalance_run_pass(const eb_model_desc* desc, int32_t N, int32_t T, float* x,
+                         const float* gain, const void* const* Wg, const float* bias,
+                         const void* const* W_gu, const void* const* W_dn, int32_t policy,
+                         int32_t m, void* state, size_t state_bytes, int32_t max_steps,
+                         int32_t* n_steps_out, uint64_t* runsets_out, int32_t* layers_out,
+                         int64_t* step_load_out, int32_t* groups_out, int32_t* layer_loads_out,
+                         void* stream);
 
 /*
  * Kernel timing for measurement.  Between easybalance_profile_begin(mask) and

@@ -22,7 +22,7 @@ EB_ERR_UNSUPPORTED = -2
 EB_ERR_HIP = -3
 EB_ERR_WORKSPACE_TOO_SMALL = -4
 EB_DTYPE_F32, EB_DTYPE_BF16 = 0, 1
-EB_POLICY_MAXUTIL, EB_POLICY_CUMUTIL, EB_POLICY_DIFFPEAK = 0, 1, 2
+EB_POLICY_MAXUTIL, EB_POLICY_CUMUTIL, EB_POLICY_DIFFPEAK, EB_POLICY_LOCKSTEP = 0, 1, 2, 3
 EB_MAX_POOL = 64
 EB_MAXUTIL_MAX_POOL = 20
 KERNEL_NAMES = ["route_norm", "route_logits", "route_topk", "perm_count", "perm_scan",
@@ -32,7 +32,8 @@ EB_PROFILE_ALL = (1 << EB_NUM_KERNELS) - 1
 
 EXPORTS = ["easybalance_version", "easybalance_last_error", "easybalance_route",
            "easybalance_schedule", "easybalance_moe_step_workspace_size", "easybalance_moe_step",
-           "easybalance_combine", "easybalance_profile_begin", "easybalance_profile_end"]
+           "easybalance_combine", "easybalance_profile_begin", "easybalance_profile_end",
+           "easybalance_pass_state_size", "easybalance_run_pass"]
 
 
 class eb_model_desc(ctypes.Structure):
@@ -88,6 +89,13 @@ def lib() -> ctypes.CDLL:
                                        ctypes.POINTER(eb_step_views), P]
     l.easybalance_combine.restype = ctypes.c_int
     l.easybalance_combine.argtypes = [D, I32, W, P, P, P, P]
+    l.easybalance_pass_state_size.restype = ctypes.c_int
+    l.easybalance_pass_state_size.argtypes = [D, I32, I32, SZP]
+    l.easybalance_run_pass.restype = ctypes.c_int
+    l.easybalance_run_pass.argtypes = [D, I32, I32, P, P, P, P, P, P, I32, I32, P, ctypes.c_size_t,
+                                       I32, ctypes.POINTER(ctypes.c_int32), U64P,
+                                       ctypes.POINTER(ctypes.c_int32), I64P,
+                                       ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32), P]
     l.easybalance_profile_begin.restype = ctypes.c_int
     l.easybalance_profile_begin.argtypes = [ctypes.c_uint32]
     l.easybalance_profile_end.restype = ctypes.c_int
@@ -187,6 +195,41 @@ def easybalance_combine(desc, run, n_run, x_list, o, inv, stream=None) -> None:
     xs = _ptr_array(x_list)
     _check("easybalance_combine", lib().easybalance_combine(
         ctypes.byref(desc), n_run, run, xs, _ptr(o), _ptr(inv), stream))
+
+
+def easybalance_pass_state_size(desc, N, T) -> int:
+    out = ctypes.c_size_t(0)
+    _check("easybalance_pass_state_size",
+           lib().easybalance_pass_state_size(ctypes.byref(desc), N, T, ctypes.byref(out)))
+    return out.value
+
+
+def easybalance_run_pass(desc, N, T, x, gain, Wg, bias, W_gu, W_dn, policy, m, state, state_bytes,
+                         max_steps=0, record=False, stream=None):
+    """Returns (n_steps, runsets [n], layers [n][N], step_load [n][D], groups [n],
+    layer_loads [N][L][D]) when record, else (n_steps, None, None, None, None, None)."""
+    n = ctypes.c_int32(0)
+    if record:
+        rs = np.zeros(max_steps, dtype=np.uint64)
+        ly = np.zeros((max_steps, N), dtype=np.int32)
+        sl = np.zeros((max_steps, desc.D), dtype=np.int64)
+        gr = np.zeros(max_steps, dtype=np.int32)
+        ll = np.zeros((N, desc.L, desc.D), dtype=np.int32)
+        ptrs = (rs.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64)),
+                ly.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                sl.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
+                gr.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                ll.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)))
+    else:
+        ptrs = (None, None, None, None, None)
+    wg, gu, dn = _ptr_array(Wg), _ptr_array(W_gu), _ptr_array(W_dn)
+    _check("easybalance_run_pass", lib().easybalance_run_pass(
+        ctypes.byref(desc), N, T, _ptr(x), _ptr(gain), wg, _ptr(bias), gu, dn, policy, m,
+        _ptr(state), state_bytes, max_steps if record else 0, ctypes.byref(n), *ptrs, stream))
+    k = min(n.value, max_steps) if record else 0
+    if not record:
+        return n.value, None, None, None, None, None
+    return n.value, rs[:k], ly[:k], sl[:k], gr[:k], ll
 
 
 def easybalance_profile_begin(kernels=None) -> None:

@@ -1,0 +1,241 @@
+// One pass of Algorithm 1 (Section 4.2) driven natively: the host loop of
+// EasyBalance over the library's own entry points.
+//
+//   route every micro-batch at layer 0                    (Attn_Route_Dispatch)
+//   while the pool is not empty:
+//     RunSet <- Schedule(pool, m)                          (the pool's expert counts)
+//     expert FFNs of RunSet jointly, then the combine      (MoECompute_Combine)
+//     l_j += 1 for j in RunSet; route those not finished
+//
+// The only host<->device synchronisation per step is the copy of the pool's
+// expert counts into pinned host memory that the scheduler needs; everything
+// else is queued on the caller's stream without waiting.
+#include <hip/hip_runtime.h>
+#include <string.h>
+
+#include <vector>
+
+#include "eb_internal.h"
+
+namespace eb {
+namespace {
+
+constexpr size_t kAlignP = 256;
+size_t align_p(size_t v) { return (v + kAlignP - 1) / kAlignP * kAlignP; }
+
+struct PassLayout {
+  size_t a, logits, idx, w, counts, o, inv, ws, ws_bytes, total;
+};
+
+PassLayout pass_layout(const eb_model_desc& d, int N, int T) {
+  const size_t eb = d.dtype == EB_DTYPE_BF16 ? 2 : 4;
+  const size_t NT = (size_t)N * T, slots = (size_t)(d.k + d.S);
+  PassLayout p{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += align_p(bytes);
+    return o;
+  };
+  p.a = take(eb * NT * d.H);
+  p.logits = take(sizeof(float) * NT * d.E);
+  p.idx = take(sizeof(int32_t) * NT * d.k);
+  p.w = take(sizeof(float) * NT * d.k);
+  p.counts = take(sizeof(int32_t) * (size_t)N * d.E);
+  p.o = take(eb * NT * slots * d.H);
+  p.inv = take(sizeof(int32_t) * NT * slots);
+  std::vector<int32_t> Ts(N, T);
+  size_t wsb = 0;
+  easybalance_moe_step_workspace_size(&d, N, Ts.data(), &wsb);
+  p.ws_bytes = wsb;
+  p.ws = take(wsb);
+  p.total = off;
+  return p;
+}
+
+// Pinned host buffer for the counts, one per host thread, grown on demand.
+struct PinnedCounts {
+  int32_t* p = nullptr;
+  size_t n = 0;
+  ~PinnedCounts() {
+    if (p) (void)hipHostFree(p);
+  }
+  int32_t* get(size_t count) {
+    if (count > n) {
+      if (p) (void)hipHostFree(p);
+      p = nullptr;
+      n = 0;
+      if (hipHostMalloc(reinterpret_cast<void**>(&p), count * sizeof(int32_t), hipHostMallocDefault) != hipSuccess)
+        return nullptr;
+      n = count;
+    }
+    return p;
+  }
+};
+thread_local PinnedCounts t_pinned;
+
+}  // namespace
+}  // namespace eb
+
+using namespace eb;
+
+extern "C" {
+
+int easybalance_pass_state_size(const eb_model_desc* desc, int32_t N, int32_t T, size_t* bytes) {
+  if (desc == nullptr || bytes == nullptr) return set_error(EB_ERR_INVALID_ARG, "desc/bytes is NULL");
+  if (N < 1 || N > EB_MAX_POOL || T < 1) return set_error(EB_ERR_INVALID_ARG, "N=%d T=%d out of range", N, T);
+  size_t wsb = 0;
+  std::vector<int32_t> Ts(N, T);
+  const int rc = easybalance_moe_step_workspace_size(desc, N, Ts.data(), &wsb);
+  if (rc) return rc;
+  *bytes = pass_layout(*desc, N, T).total;
+  return EB_OK;
+}
+
+int easybalance_run_pass(const eb_model_desc* desc, int32_t N, int32_t T, float* x,
+                         const float* gain, const void* const* Wg, const float* bias,
+                         const void* const* W_gu, const void* const* W_dn, int32_t policy,
+                         int32_t m, void* state, size_t state_bytes, int32_t max_steps,
+                         int32_t* n_steps_out, uint64_t* runsets_out, int32_t* layers_out,
+                         int64_t* step_load_out, int32_t* groups_out, int32_t* layer_loads_out,
+                         void* stream) {
+  size_t need = 0;
+  int rc = easybalance_pass_state_size(desc, N, T, &need);
+  if (rc) return rc;
+  const eb_model_desc& d = *desc;
+  if (x == nullptr || gain == nullptr || Wg == nullptr || bias == nullptr || W_gu == nullptr ||
+      W_dn == nullptr)
+    return set_error(EB_ERR_INVALID_ARG, "a required pass pointer is NULL");
+  if (policy < EB_POLICY_MAXUTIL || policy > EB_POLICY_LOCKSTEP)
+    return set_error(EB_ERR_INVALID_ARG, "policy %d unknown", policy);
+  if (policy == EB_POLICY_MAXUTIL && N > EB_MAXUTIL_MAX_POOL)
+    return set_error(EB_ERR_UNSUPPORTED, "MaxUtil enumerates subsets of at most %d micro-batches",
+                     EB_MAXUTIL_MAX_POOL);
+  if (m < 1) return set_error(EB_ERR_INVALID_ARG, "m=%d < 1", m);
+  if (state == nullptr || (reinterpret_cast<uintptr_t>(state) % kAlignP) != 0)
+    return set_error(EB_ERR_INVALID_ARG, "state must be non-NULL and 256-byte aligned");
+  if (state_bytes < need)
+    return set_error(EB_ERR_WORKSPACE_TOO_SMALL, "state %zu < %zu bytes", state_bytes, need);
+  if (max_steps < 0 || ((runsets_out || layers_out || step_load_out || groups_out) && max_steps == 0))
+    return set_error(EB_ERR_INVALID_ARG, "max_steps=%d", max_steps);
+
+  const PassLayout P = pass_layout(d, N, T);
+  uint8_t* base = static_cast<uint8_t*>(state);
+  const size_t eb = d.dtype == EB_DTYPE_BF16 ? 2 : 4;
+  auto a_of = [&](int j) { return base + P.a + eb * (size_t)j * T * d.H; };
+  auto logits_of = [&](int j) { return reinterpret_cast<float*>(base + P.logits) + (size_t)j * T * d.E; };
+  auto idx_of = [&](int j) { return reinterpret_cast<int32_t*>(base + P.idx) + (size_t)j * T * d.k; };
+  auto w_of = [&](int j) { return reinterpret_cast<float*>(base + P.w) + (size_t)j * T * d.k; };
+  int32_t* counts_dev = reinterpret_cast<int32_t*>(base + P.counts);
+  auto x_of = [&](int j) { return x + (size_t)j * T * d.H; };
+  void* o = base + P.o;
+  int32_t* inv = reinterpret_cast<int32_t*>(base + P.inv);
+  void* ws = base + P.ws;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+
+  int32_t* counts = t_pinned.get((size_t)N * d.E);
+  if (counts == nullptr) return set_error(EB_ERR_HIP, "pinned host allocation failed");
+  const int per = d.E / d.D;
+  if (layer_loads_out) {
+    for (size_t i = 0; i < (size_t)N * d.L * d.D; ++i) layer_loads_out[i] = -1;
+  }
+
+  auto route = [&](int j, int l) {
+    return easybalance_route(desc, l, T, x_of(j), gain + (size_t)l * d.H, Wg[l], bias + (size_t)l * d.E,
+                             a_of(j), logits_of(j), idx_of(j), w_of(j), counts_dev + (size_t)j * d.E,
+                             stream);
+  };
+  std::vector<int32_t> layer(N, 0), pool(N);
+  for (int j = 0; j < N; ++j) {
+    pool[j] = j;
+    if ((rc = route(j, 0))) return rc;
+  }
+  std::vector<int32_t> pool_counts;
+  std::vector<int64_t> load(d.D);
+  std::vector<eb_work> run;
+  std::vector<float*> xs;
+  int n_steps = 0;
+  while (!pool.empty()) {
+    if (hipMemcpyAsync(counts, counts_dev, sizeof(int32_t) * (size_t)N * d.E, hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess)
+      return set_error(EB_ERR_HIP, "counts copy: %s", hipGetErrorString(hipGetLastError()));
+    const int n_pool = (int)pool.size();
+    if (layer_loads_out) {
+      for (int j : pool)
+        for (int dv = 0; dv < d.D; ++dv) {
+          int64_t sum = 0;
+          for (int e = dv * per; e < (dv + 1) * per; ++e) sum += counts[(size_t)j * d.E + e];
+          layer_loads_out[((size_t)j * d.L + layer[j]) * d.D + dv] = (int32_t)sum;
+        }
+    }
+    uint64_t mask = 0;
+    if (policy == EB_POLICY_LOCKSTEP) {
+      for (int dv = 0; dv < d.D; ++dv) load[dv] = 0;
+      for (int j : pool) {
+        mask |= 1ull << j;
+        for (int e = 0; e < d.E; ++e) load[e / per] += counts[(size_t)j * d.E + e];
+      }
+    } else {
+      pool_counts.resize((size_t)n_pool * d.E);
+      for (int i = 0; i < n_pool; ++i)
+        memcpy(&pool_counts[(size_t)i * d.E], counts + (size_t)pool[i] * d.E, sizeof(int32_t) * d.E);
+      if ((rc = schedule_impl(n_pool, pool.data(), pool_counts.data(), d.E, d.D, m, policy, &mask,
+                              load.data())))
+        return rc;
+    }
+    run.clear();
+    xs.clear();
+    for (int j : pool)
+      if ((mask >> j) & 1) {
+        run.push_back(eb_work{j, layer[j], T, 0, a_of(j), idx_of(j), w_of(j)});
+        xs.push_back(x_of(j));
+      }
+    if (n_steps < max_steps) {
+      if (runsets_out) runsets_out[n_steps] = mask;
+      if (layers_out)
+        for (int j = 0; j < N; ++j) layers_out[(size_t)n_steps * N + j] = ((mask >> j) & 1) ? layer[j] : -1;
+      if (step_load_out)
+        for (int dv = 0; dv < d.D; ++dv) step_load_out[(size_t)n_steps * d.D + dv] = load[dv];
+      if (groups_out) {
+        // distinct (layer, expert) keys with a token among the RunSet's entries
+        std::vector<uint8_t> seen((size_t)d.L * d.E, 0);
+        std::vector<uint8_t> layer_seen(d.L, 0);
+        int g = 0;
+        for (const eb_work& r : run) {
+          if (!layer_seen[r.layer]) {
+            layer_seen[r.layer] = 1;
+            g += d.S;
+          }
+          for (int e = 0; e < d.E; ++e)
+            if (counts[(size_t)r.mb_id * d.E + e] > 0 && !seen[(size_t)r.layer * d.E + e]) {
+              seen[(size_t)r.layer * d.E + e] = 1;
+              ++g;
+            }
+        }
+        groups_out[n_steps] = g;
+      }
+    }
+    ++n_steps;
+    const int n_run = (int)run.size();
+    if ((rc = easybalance_moe_step(desc, n_run, run.data(), W_gu, W_dn, ws, P.ws_bytes, o, inv,
+                                   nullptr, stream)))
+      return rc;
+    if ((rc = easybalance_combine(desc, n_run, run.data(), xs.data(), o, inv, stream))) return rc;
+    std::vector<int32_t> next;
+    for (int j : pool) {
+      if ((mask >> j) & 1) {
+        if (++layer[j] < d.L) {
+          if ((rc = route(j, layer[j]))) return rc;
+          next.push_back(j);
+        }
+      } else {
+        next.push_back(j);
+      }
+    }
+    pool.swap(next);
+  }
+  if (n_steps_out) *n_steps_out = n_steps;
+  return EB_OK;
+}
+
+}  // extern "C"

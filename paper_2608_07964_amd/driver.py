@@ -83,6 +83,35 @@ class Stack:
         B.easybalance_combine(self.desc, run, len(runset), [self.x[j] for j, _ in runset],
                               self.o, self.inv, stream)
 
+    # ---- Algorithm 1, natively ----------------------------------------------
+    def run_native(self, policy: str = "maxutil", m: int | None = None, record: bool = True,
+                   stream=None) -> list[StepRecord]:
+        """The same pass as run(), driven by easybalance_run_pass (the host
+        loop in the library).  Fills layer_loads and returns the steps when
+        record (records cover the first N*L steps, i.e. all of them)."""
+        if stream is None:
+            stream = torch.cuda.current_stream(self.dev)
+        pol = B.EB_POLICY_LOCKSTEP if policy == "lockstep" else POLICIES[policy]
+        m = self.N if m is None else m
+        if not hasattr(self, "_state"):
+            self._state_bytes = B.easybalance_pass_state_size(self.desc, self.N, self.T)
+            self._state = torch.empty(self._state_bytes + 256, dtype=torch.uint8, device=self.dev)
+        sp = self._state.data_ptr() + (-self._state.data_ptr()) % 256
+        n, rs, ly, sl, gr, ll = B.easybalance_run_pass(
+            self.desc, self.N, self.T, self.x, self.gain, self.Wg, self.bias, self.W_gu, self.W_dn,
+            pol, m, sp, self._state_bytes, max_steps=self.N * self.L, record=record,
+            stream=stream.cuda_stream)
+        if not record:
+            return []
+        self.layer_loads = ll.astype(np.int64)
+        steps = []
+        for i in range(n):
+            runset = [(j, int(ly[i, j])) for j in range(self.N) if (int(rs[i]) >> j) & 1]
+            steps.append(StepRecord(runset=runset, load=sl[i].copy(),
+                                    pairs=len(runset) * self.T * (self.k + self.S),
+                                    groups=int(gr[i])))
+        return steps
+
     # ---- Algorithm 1 --------------------------------------------------------
     def run(self, policy: str = "maxutil", m: int | None = None, record: bool = True,
             stream=None, views=None, hook=None) -> list[StepRecord]:

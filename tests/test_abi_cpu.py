@@ -126,3 +126,27 @@ def test_device_calls_reject_bad_arguments_before_touching_the_gpu():
         B.easybalance_moe_step(d, run, 1, [1, 1], [1, 1], 255, 1 << 30, 1, 1)  # misaligned
     with pytest.raises(B.EasyBalanceError):
         B.easybalance_combine(d, run, 0, [1], 1, 1)                     # n_run = 0
+
+
+def test_run_pass_rejects_bad_arguments_before_touching_the_gpu():
+    d = B.make_desc(2, 256, 128, 8, 2, 0, 4, "bf16")
+    need = B.easybalance_pass_state_size(d, 4, 64)
+    assert need > 0
+    with pytest.raises(B.EasyBalanceError):
+        B.easybalance_pass_state_size(d, 0, 64)
+    with pytest.raises(B.EasyBalanceError):
+        B.easybalance_pass_state_size(d, 65, 64)
+    fake = 1 << 20  # non-NULL, 256-byte aligned; never dereferenced on these paths
+    args = (d, 4, 64, fake, fake, [fake, fake], fake, [fake, fake], [fake, fake])
+    with pytest.raises(B.EasyBalanceError) as e:   # state too small
+        B.easybalance_run_pass(*args, B.EB_POLICY_MAXUTIL, 3, fake, need - 1)
+    assert e.value.code == B.EB_ERR_WORKSPACE_TOO_SMALL
+    with pytest.raises(B.EasyBalanceError) as e:   # unknown policy
+        B.easybalance_run_pass(*args, 7, 3, fake, need)
+    assert e.value.code == B.EB_ERR_INVALID_ARG
+    with pytest.raises(B.EasyBalanceError) as e:   # misaligned state
+        B.easybalance_run_pass(*args, B.EB_POLICY_MAXUTIL, 3, fake + 4, need)
+    assert e.value.code == B.EB_ERR_INVALID_ARG
+    with pytest.raises(B.EasyBalanceError) as e:   # m < 1
+        B.easybalance_run_pass(*args, B.EB_POLICY_MAXUTIL, 0, fake, need)
+    assert e.value.code == B.EB_ERR_INVALID_ARG

@@ -1,0 +1,46 @@
+"""The native Algorithm-1 driver (easybalance_run_pass) against the Python
+driver over the same entry points: identical schedules, loads, group counts
+and bit-identical hidden states, for every policy, on the small stacks and on
+the full-size Mixtral-shaped stack that bench.py times."""
+import numpy as np
+import pytest
+import torch
+
+from synth import CONFIGS, mini
+from synth.device import DeviceInputs
+
+from gpu_helpers import log, make_stack
+
+pytestmark = pytest.mark.gpu
+
+SMALL = [CONFIGS[0]] + [mini(c) for c in CONFIGS[1:]] + [mini(CONFIGS[1], H=256, F=8192, T=96, L=2)]
+SMALL_IDS = [c.name for c in SMALL[:-1]] + [SMALL[-1].name + "_longk"]
+
+
+def _compare(cfg, device, policies):
+    inp = DeviceInputs(cfg, device)
+    for policy, m in policies:
+        st, _ = make_stack(cfg, device, inputs=inp)
+        py_steps = st.run(policy, m=m)
+        torch.cuda.synchronize()
+        x_py, ll_py = st.x.clone(), st.layer_loads.copy()
+        st.x.copy_(inp.x0)
+        nat_steps = st.run_native(policy, m=m)
+        torch.cuda.synchronize()
+        assert torch.equal(st.x, x_py), (policy, m)
+        assert np.array_equal(st.layer_loads, ll_py), (policy, m)
+        assert [s.runset for s in nat_steps] == [s.runset for s in py_steps], (policy, m)
+        for a, b in zip(nat_steps, py_steps):
+            assert np.array_equal(a.load, b.load) and a.groups == b.groups and a.pairs == b.pairs
+        log(f"  {cfg.name} {policy} m={m}: {len(nat_steps)} steps identical")
+
+
+@pytest.mark.parametrize("cfg", SMALL, ids=SMALL_IDS)
+def test_native_pass_matches_python_driver(cfg, device):
+    _compare(cfg, device, [("maxutil", cfg.m), ("maxutil", 1), ("cumutil", cfg.m),
+                           ("diffpeak", cfg.m), ("lockstep", None)])
+
+
+def test_native_pass_full_size_bench_stack(device):
+    cfg = [c for c in CONFIGS if c.name == "mixtral_bf16"][0]
+    _compare(cfg, device, [("maxutil", cfg.m), ("lockstep", None)])
