@@ -62,7 +62,30 @@ __device__ __forceinline__ int find_entry(const int32_t* base, int n, int v) {
   return lo;
 }
 
+// Routing of up to kRouteBatch micro-batches in one set of launches: entry i
+// holds tokens tok0[i] .. tok0[i+1]-1 of the batch and 32-token blocks
+// blk0[i] .. blk0[i+1]-1; gain/Wg/bias are those of the entry's layer.
+constexpr int kRouteBatch = 32;
+struct RouteEntry {
+  const float* x;
+  const float* gain;
+  const void* Wg;
+  const float* bias;
+  void* a;
+  float* z;
+  int32_t* idx;
+  float* w;
+  int32_t* counts;
+};
+struct RouteBatch {
+  int32_t n;
+  int32_t tok0[kRouteBatch + 1];
+  int32_t blk0[kRouteBatch + 1];
+  RouteEntry e[kRouteBatch];
+};
+
 // ---- launchers (return hipError_t of the launch) ---------------------------
+hipError_t launch_route_batch(const eb_model_desc& d, const RouteBatch& rb, hipStream_t s);
 hipError_t launch_route(const eb_model_desc& d, int T, const float* x, const float* gain,
                         const void* Wg, const float* bias, void* a_out, float* logits,
                         int32_t* idx, float* w, int32_t* counts, hipStream_t s);

@@ -13,6 +13,7 @@
 #include <hip/hip_runtime.h>
 #include <string.h>
 
+#include <algorithm>
 #include <vector>
 
 #include "eb_internal.h"
@@ -140,16 +141,31 @@ int easybalance_run_pass(const eb_model_desc* desc, int32_t N, int32_t T, float*
     for (size_t i = 0; i < (size_t)N * d.L * d.D; ++i) layer_loads_out[i] = -1;
   }
 
-  auto route = [&](int j, int l) {
-    return easybalance_route(desc, l, T, x_of(j), gain + (size_t)l * d.H, Wg[l], bias + (size_t)l * d.E,
-                             a_of(j), logits_of(j), idx_of(j), w_of(j), counts_dev + (size_t)j * d.E,
-                             stream);
-  };
+  for (int l = 0; l < d.L; ++l)
+    if (Wg[l] == nullptr || W_gu[l] == nullptr || W_dn[l] == nullptr)
+      return set_error(EB_ERR_INVALID_ARG, "weights of layer %d are NULL", l);
   std::vector<int32_t> layer(N, 0), pool(N);
-  for (int j = 0; j < N; ++j) {
-    pool[j] = j;
-    if ((rc = route(j, 0))) return rc;
-  }
+  // routes micro-batches js (each at its layer) in batches of kRouteBatch
+  auto route = [&](const std::vector<int32_t>& js) -> int {
+    for (size_t b = 0; b < js.size(); b += kRouteBatch) {
+      RouteBatch rb;
+      rb.n = (int)std::min<size_t>(kRouteBatch, js.size() - b);
+      rb.tok0[0] = 0;
+      rb.blk0[0] = 0;
+      for (int i = 0; i < rb.n; ++i) {
+        const int j = js[b + i], l = layer[j];
+        rb.tok0[i + 1] = rb.tok0[i] + T;
+        rb.blk0[i + 1] = rb.blk0[i] + (T + 31) / 32;
+        rb.e[i] = RouteEntry{x_of(j), gain + (size_t)l * d.H, Wg[l], bias + (size_t)l * d.E, a_of(j),
+                             logits_of(j), idx_of(j), w_of(j), counts_dev + (size_t)j * d.E};
+      }
+      const hipError_t e = launch_route_batch(d, rb, s);
+      if (e != hipSuccess) return set_error(EB_ERR_HIP, "route launch: %s", hipGetErrorString(e));
+    }
+    return EB_OK;
+  };
+  for (int j = 0; j < N; ++j) pool[j] = j;
+  if ((rc = route(pool))) return rc;
   std::vector<int32_t> pool_counts;
   std::vector<int64_t> load(d.D);
   std::vector<eb_work> run;
@@ -221,17 +237,18 @@ int easybalance_run_pass(const eb_model_desc* desc, int32_t N, int32_t T, float*
                                    nullptr, stream)))
       return rc;
     if ((rc = easybalance_combine(desc, n_run, run.data(), xs.data(), o, inv, stream))) return rc;
-    std::vector<int32_t> next;
+    std::vector<int32_t> next, advanced;
     for (int j : pool) {
       if ((mask >> j) & 1) {
         if (++layer[j] < d.L) {
-          if ((rc = route(j, layer[j]))) return rc;
+          advanced.push_back(j);
           next.push_back(j);
         }
       } else {
         next.push_back(j);
       }
     }
+    if ((rc = route(advanced))) return rc;
     pool.swap(next);
   }
   if (n_steps_out) *n_steps_out = n_steps;

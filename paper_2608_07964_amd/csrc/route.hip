@@ -10,7 +10,10 @@
 //   rmsnorm_kernel +     other fp32 stacks: RMSNorm, an LDS-tiled fp32
 //   logits_kernel +      VALU GEMM for z, then the top-k
 //   topk_kernel
-//   counts_kernel        expert counts of the micro-batch from its picks
+//   counts_kernel        expert counts of each micro-batch from its picks
+// Every kernel takes a batch of micro-batches (possibly at different layers)
+// and finds its entry from its block index, so routing several micro-batches
+// costs one set of launches.
 // Every reduction runs in a fixed order, so a token's routing depends on its
 // own inputs only (not on the other tokens of the launch).
 #include <math.h>
@@ -65,12 +68,15 @@ __device__ __forceinline__ float4 normed(float4 v, float r, float4 g) {
 // ---------------------------------------------------------------------------
 // RMSNorm + cast, one wavefront per token.
 template <typename TA>
-__global__ __launch_bounds__(256) void rmsnorm_kernel(int T, int H, const float* __restrict__ x,
-                                                      const float* __restrict__ gain,
-                                                      TA* __restrict__ a, float eps) {
+__global__ __launch_bounds__(256) void rmsnorm_kernel(RouteBatch rb, int H, float eps) {
   const int lane = threadIdx.x & 63;
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= T) return;
+  const int g = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (g >= rb.tok0[rb.n]) return;
+  const int ei = find_entry(rb.tok0, rb.n, g);
+  const int t = g - rb.tok0[ei];
+  const float* __restrict__ x = rb.e[ei].x;
+  const float* __restrict__ gain = rb.e[ei].gain;
+  TA* __restrict__ a = static_cast<TA*>(rb.e[ei].a);
   const float4* xr = reinterpret_cast<const float4*>(x + (size_t)t * H);
   const float4* g4 = reinterpret_cast<const float4*>(gain);
   const int n4 = H >> 2;
@@ -219,10 +225,14 @@ __device__ __forceinline__ void topk_group8(int sub, int E, int k, int norm_topk
   }
 }
 
-// Expert counts of the micro-batch from its picks, by one workgroup (an LDS
-// histogram, then one plain store per expert: nothing to clear beforehand).
-__global__ __launch_bounds__(1024) void counts_kernel(int n, int E, const int32_t* __restrict__ idx,
-                                                      int32_t* __restrict__ counts) {
+// Expert counts of a micro-batch from its picks, one workgroup per batch entry
+// (an LDS histogram, then one plain store per expert: nothing to clear
+// beforehand; an entry without tokens gets zeros).
+__global__ __launch_bounds__(1024) void counts_kernel(RouteBatch rb, int k, int E) {
+  const int ei = blockIdx.x;
+  const int n = (rb.tok0[ei + 1] - rb.tok0[ei]) * k;
+  const int32_t* __restrict__ idx = rb.e[ei].idx;
+  int32_t* __restrict__ counts = rb.e[ei].counts;
   __shared__ int hist[1024];
   for (int e = threadIdx.x; e < E; e += blockDim.x) hist[e] = 0;
   __syncthreads();
@@ -335,15 +345,21 @@ constexpr int kTokChunks = 4;  // 8-element chunks per thread: H <= 256 * 8 * 4
 constexpr int kTokMaxH = 256 * 8 * kTokChunks;
 
 template <typename TA, int EMAX>
-__global__ __launch_bounds__(256) void route_token_kernel(
-    int T, int H, int E, int k, int norm_topk, const float* __restrict__ x,
-    const float* __restrict__ gain, const TA* __restrict__ Wg, const float* __restrict__ bias,
-    TA* __restrict__ a, float* __restrict__ z, int32_t* __restrict__ idx, float* __restrict__ w,
-    float eps) {
+__global__ __launch_bounds__(256) void route_token_kernel(RouteBatch rb, int H, int E, int k,
+                                                          int norm_topk, float eps) {
   __shared__ float red[4];
   __shared__ float red_z[4][EMAX + 1];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int t = blockIdx.x;
+  const int ei = find_entry(rb.tok0, rb.n, blockIdx.x);
+  const int t = blockIdx.x - rb.tok0[ei];
+  const float* __restrict__ x = rb.e[ei].x;
+  const float* __restrict__ gain = rb.e[ei].gain;
+  const TA* __restrict__ Wg = static_cast<const TA*>(rb.e[ei].Wg);
+  const float* __restrict__ bias = rb.e[ei].bias;
+  TA* __restrict__ a = static_cast<TA*>(rb.e[ei].a);
+  float* __restrict__ z = rb.e[ei].z;
+  int32_t* __restrict__ idx = rb.e[ei].idx;
+  float* __restrict__ w = rb.e[ei].w;
   const float* xr = x + (size_t)t * H;
   const int nchunk = H >> 3;
   // thread tid owns chunks c = tid + 256 i (8 elements each), kept in registers
@@ -424,19 +440,22 @@ __global__ __launch_bounds__(256) void route_token_kernel(
 // summation order), and writes the logits to z and to an LDS tile from which
 // 8 lanes per token pick its top-k.
 template <int NB>
-__global__ __launch_bounds__(256) void route_mfma_kernel(int T, int H, int E, int k, int norm_topk,
-                                                         const bf16_t* __restrict__ a,
-                                                         const bf16_t* __restrict__ Wg,
-                                                         const float* __restrict__ bias,
-                                                         float* __restrict__ z,
-                                                         int32_t* __restrict__ idx,
-                                                         float* __restrict__ w) {
+__global__ __launch_bounds__(256) void route_mfma_kernel(RouteBatch rb, int H, int E, int k,
+                                                         int norm_topk) {
   constexpr int ZS = NB * 32 + 1;  // padded LDS row of the logit tile
   __shared__ float part[3][NB][16][64];
   __shared__ float zs[32][ZS];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lrow = lane & 31, khalf = lane >> 5;
-  const int t0 = blockIdx.x * 32;
+  const int ei = find_entry(rb.blk0, rb.n, blockIdx.x);
+  const int T = rb.tok0[ei + 1] - rb.tok0[ei];
+  const int t0 = (blockIdx.x - rb.blk0[ei]) * 32;
+  const bf16_t* __restrict__ a = static_cast<const bf16_t*>(rb.e[ei].a);
+  const bf16_t* __restrict__ Wg = static_cast<const bf16_t*>(rb.e[ei].Wg);
+  const float* __restrict__ bias = rb.e[ei].bias;
+  float* __restrict__ z = rb.e[ei].z;
+  int32_t* __restrict__ idx = rb.e[ei].idx;
+  float* __restrict__ w = rb.e[ei].w;
   const int kq = H / 4, kbeg = wave * kq;
   // this lane's A row (token) and B rows (experts), clamped into range
   const bf16_t* arow = a + (size_t)min(t0 + lrow, T - 1) * H + kbeg + 8 * khalf;
@@ -529,77 +548,82 @@ __global__ __launch_bounds__(256) void topk_kernel(int T, int E, int k, int norm
   topk_token(E, k, norm_topk, [&](int e) { return zr[e]; }, idx + (size_t)t * k, w + (size_t)t * k);
 }
 
-__global__ void zero_i32_kernel(int32_t* p, int n) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) p[i] = 0;
-}
-
 template <typename TA>
-hipError_t route_typed(const eb_model_desc& d, int T, const float* x, const float* gain,
-                       const void* Wg, const float* bias, void* a_out, float* logits,
-                       int32_t* idx, float* w, int32_t* counts, hipStream_t s) {
-  if (T == 0) {
-    hipLaunchKernelGGL(zero_i32_kernel, dim3((d.E + 255) / 256), dim3(256), 0, s, counts, d.E);
-    return hipGetLastError();
-  }
-  const bool fused_token = (sizeof(TA) == 2 ? d.E <= 8 : d.E <= 64) && d.H <= kTokMaxH;
-  if (fused_token) {
-    prof_start(EB_K_ROUTE_LOGITS, s);
-    if (d.E <= 8)
-      hipLaunchKernelGGL((route_token_kernel<TA, 8>), dim3(T), dim3(256), 0, s, T, d.H, d.E, d.k,
-                         d.norm_topk, x, gain, static_cast<const TA*>(Wg), bias,
-                         static_cast<TA*>(a_out), logits, idx, w, d.rms_eps);
-    else
-      hipLaunchKernelGGL((route_token_kernel<TA, 64>), dim3(T), dim3(256), 0, s, T, d.H, d.E, d.k,
-                         d.norm_topk, x, gain, static_cast<const TA*>(Wg), bias,
-                         static_cast<TA*>(a_out), logits, idx, w, d.rms_eps);
-    prof_stop(EB_K_ROUTE_LOGITS, s);
-  } else {
-    prof_start(EB_K_ROUTE_NORM, s);
-    hipLaunchKernelGGL(rmsnorm_kernel<TA>, dim3((T + 3) / 4), dim3(256), 0, s, T, d.H, x, gain,
-                       static_cast<TA*>(a_out), d.rms_eps);
-    prof_stop(EB_K_ROUTE_NORM, s);
-    prof_start(EB_K_ROUTE_LOGITS, s);
-    if (sizeof(TA) == 2) {
-      const dim3 grid((T + 31) / 32);
-      const bf16_t* ab = static_cast<const bf16_t*>(a_out);
-      const bf16_t* wb = static_cast<const bf16_t*>(Wg);
-      const int nb = (d.E + 31) / 32;
-      if (nb <= 2)
-        hipLaunchKernelGGL(route_mfma_kernel<2>, grid, dim3(256), 0, s, T, d.H, d.E, d.k,
-                           d.norm_topk, ab, wb, bias, logits, idx, w);
-      else if (nb <= 4)
-        hipLaunchKernelGGL(route_mfma_kernel<4>, grid, dim3(256), 0, s, T, d.H, d.E, d.k,
-                           d.norm_topk, ab, wb, bias, logits, idx, w);
+hipError_t route_batch_typed(const eb_model_desc& d, const RouteBatch& rb, hipStream_t s) {
+  const int total = rb.tok0[rb.n];
+  if (total > 0) {
+    const bool fused_token = (sizeof(TA) == 2 ? d.E <= 8 : d.E <= 64) && d.H <= kTokMaxH;
+    if (fused_token) {
+      prof_start(EB_K_ROUTE_LOGITS, s);
+      if (d.E <= 8)
+        hipLaunchKernelGGL((route_token_kernel<TA, 8>), dim3(total), dim3(256), 0, s, rb, d.H, d.E,
+                           d.k, d.norm_topk, d.rms_eps);
       else
-        hipLaunchKernelGGL(route_mfma_kernel<8>, grid, dim3(256), 0, s, T, d.H, d.E, d.k,
-                           d.norm_topk, ab, wb, bias, logits, idx, w);
+        hipLaunchKernelGGL((route_token_kernel<TA, 64>), dim3(total), dim3(256), 0, s, rb, d.H,
+                           d.E, d.k, d.norm_topk, d.rms_eps);
       prof_stop(EB_K_ROUTE_LOGITS, s);
     } else {
-      hipLaunchKernelGGL(logits_kernel<TA>, dim3((T + LG_BT - 1) / LG_BT, (d.E + LG_BE - 1) / LG_BE),
-                         dim3(256), 0, s, T, d.H, d.E, static_cast<const TA*>(a_out),
-                         static_cast<const TA*>(Wg), bias, logits);
-      prof_stop(EB_K_ROUTE_LOGITS, s);
-      prof_start(EB_K_ROUTE_TOPK, s);
-      hipLaunchKernelGGL(topk_kernel, dim3((T + 255) / 256), dim3(256), 0, s, T, d.E, d.k,
-                         d.norm_topk, logits, idx, w);
-      prof_stop(EB_K_ROUTE_TOPK, s);
+      prof_start(EB_K_ROUTE_NORM, s);
+      hipLaunchKernelGGL(rmsnorm_kernel<TA>, dim3((total + 3) / 4), dim3(256), 0, s, rb, d.H,
+                         d.rms_eps);
+      prof_stop(EB_K_ROUTE_NORM, s);
+      prof_start(EB_K_ROUTE_LOGITS, s);
+      if (sizeof(TA) == 2) {
+        const dim3 grid(rb.blk0[rb.n]);
+        const int nb = (d.E + 31) / 32;
+        if (nb <= 2)
+          hipLaunchKernelGGL(route_mfma_kernel<2>, grid, dim3(256), 0, s, rb, d.H, d.E, d.k, d.norm_topk);
+        else if (nb <= 4)
+          hipLaunchKernelGGL(route_mfma_kernel<4>, grid, dim3(256), 0, s, rb, d.H, d.E, d.k, d.norm_topk);
+        else
+          hipLaunchKernelGGL(route_mfma_kernel<8>, grid, dim3(256), 0, s, rb, d.H, d.E, d.k, d.norm_topk);
+        prof_stop(EB_K_ROUTE_LOGITS, s);
+      } else {
+        for (int i = 0; i < rb.n; ++i) {
+          const int T = rb.tok0[i + 1] - rb.tok0[i];
+          if (T == 0) continue;
+          const RouteEntry& e = rb.e[i];
+          hipLaunchKernelGGL(logits_kernel<TA>, dim3((T + LG_BT - 1) / LG_BT, (d.E + LG_BE - 1) / LG_BE),
+                             dim3(256), 0, s, T, d.H, d.E, static_cast<const TA*>(e.a),
+                             static_cast<const TA*>(e.Wg), e.bias, e.z);
+        }
+        prof_stop(EB_K_ROUTE_LOGITS, s);
+        prof_start(EB_K_ROUTE_TOPK, s);
+        for (int i = 0; i < rb.n; ++i) {
+          const int T = rb.tok0[i + 1] - rb.tok0[i];
+          if (T == 0) continue;
+          const RouteEntry& e = rb.e[i];
+          hipLaunchKernelGGL(topk_kernel, dim3((T + 255) / 256), dim3(256), 0, s, T, d.E, d.k,
+                             d.norm_topk, e.z, e.idx, e.w);
+        }
+        prof_stop(EB_K_ROUTE_TOPK, s);
+      }
     }
   }
   prof_start(EB_K_ROUTE_TOPK, s);
-  hipLaunchKernelGGL(counts_kernel, dim3(1), dim3(1024), 0, s, T * d.k, d.E, idx, counts);
+  hipLaunchKernelGGL(counts_kernel, dim3(rb.n), dim3(1024), 0, s, rb, d.k, d.E);
   prof_stop(EB_K_ROUTE_TOPK, s);
   return hipGetLastError();
 }
 
 }  // namespace
 
+hipError_t launch_route_batch(const eb_model_desc& d, const RouteBatch& rb, hipStream_t s) {
+  if (d.dtype == EB_DTYPE_BF16) return route_batch_typed<bf16_t>(d, rb, s);
+  return route_batch_typed<float>(d, rb, s);
+}
+
 hipError_t launch_route(const eb_model_desc& d, int T, const float* x, const float* gain,
                         const void* Wg, const float* bias, void* a_out, float* logits,
                         int32_t* idx, float* w, int32_t* counts, hipStream_t s) {
-  if (d.dtype == EB_DTYPE_BF16)
-    return route_typed<bf16_t>(d, T, x, gain, Wg, bias, a_out, logits, idx, w, counts, s);
-  return route_typed<float>(d, T, x, gain, Wg, bias, a_out, logits, idx, w, counts, s);
+  RouteBatch rb;
+  rb.n = 1;
+  rb.tok0[0] = 0;
+  rb.tok0[1] = T;
+  rb.blk0[0] = 0;
+  rb.blk0[1] = (T + 31) / 32;
+  rb.e[0] = RouteEntry{x, gain, Wg, bias, a_out, logits, idx, w, counts};
+  return launch_route_batch(d, rb, s);
 }
 
 }  // namespace eb
