@@ -7,11 +7,11 @@
 //   gate/up:  h = dtype( SiLU(A Wgate^T) * (A Wup^T) )   A [P][H], W_gu[l][e] [2F][H]
 //   down:     o = dtype( h Wdown^T )                     h [P][F], W_dn[l][e] [H][F]
 //
-// bf16 path: MFMA v_mfma_f32_32x32x16_bf16, 256x256 output tile per
-// workgroup of 4 wavefronts (128x128 each), K step 64 double-buffered in LDS,
-// filled by buffer loads straight into LDS (XOR-swizzled 16-byte chunks) one
-// stage ahead of the MFMAs; persistent, XCD-aware work distribution.  The gate/up B tile
-// interleaves 64 gate rows and the 64 matching up rows per wavefront column,
+// bf16 path: MFMA v_mfma_f32_32x32x16_bf16, up to 256x256 outputs per
+// workgroup of 8 wavefronts, K stages of 64 in LDS rings filled by buffer
+// loads straight into LDS (XOR-swizzled 16-byte chunks) several stages ahead
+// of the MFMAs; persistent, XCD-aware work distribution.  The gate/up B tile
+// interleaves the gate rows and the matching up rows per wavefront column,
 // so each lane holds gate and up of the same (row, f) and SwiGLU runs in
 // registers.
 //
@@ -32,8 +32,8 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 enum { MODE_GATEUP = 0, MODE_DOWN = 1 };
 
-// bf16 tiles.  Every tile is BM x 256 outputs on a workgroup of 4 wavefronts
-// (one per SIMD) and K advances 64 at a time, so every 128-byte line of A and
+// bf16 tiles.  Every tile is BM x 256 outputs on a workgroup of 8 wavefronts
+// (two per SIMD) and K advances 64 at a time, so every 128-byte line of A and
 // B is consumed whole by one stage; stages are filled by buffer loads straight
 // into LDS.  The B tile (256 weight rows x 64 k) is the same in every shape;
 // the shape of an m-tile follows the rows it holds:
@@ -43,13 +43,13 @@ enum { MODE_GATEUP = 0, MODE_DOWN = 1 };
 //   BM 128 (65..128 rows): 2 x 4 wavefronts of 64 x 64, 3 stages of A and B;
 //   BM 64  (<= 64 rows): 2 x 4 wavefronts of 32 x 64, 4 stages of A and B.
 //
-// Eight wavefronts (two per SIMD) keep each matrix core fed while the other
-// wavefront of its SIMD waits on a barrier or on LDS.  Groups that run few
-// m-tiles are bound by streaming their expert's weights from HBM, which needs
-// many bytes in flight per CU: every shape keeps at least two B stages in
-// flight.  Fragments of the next k-step are read while the MFMAs of the
-// current one run, and the per-stage barrier sits before the last k-step's
-// MFMAs.
+// Two wavefronts per SIMD keep each matrix core fed while the other one
+// waits on a barrier or on LDS.  Groups that run few m-tiles are bound by
+// streaming their expert's weights from HBM, which needs many bytes in flight
+// per CU: every shape keeps at least two B stages in flight.  Fragments of the
+// next k-step are read while the MFMAs of the current one run (every
+// instruction's place in the k-step is fixed, see kstep), and the per-stage
+// barrier sits before the last k-step's MFMAs.
 constexpr int BN = 256, BK = 64;
 constexpr int kWaves = 8;                        // two wavefronts per SIMD
 constexpr int kThreads = 64 * kWaves;
@@ -138,27 +138,32 @@ struct Frags {
   bf16x8 a[C::MB], b[C::NB];
 };
 
-// Loads of stage s (K columns 64 s .. 64 s + 63) of A into A slot sa and of
-// B into B slot sb.
+// Load j of the wave's A resp. B loads of stage s (K columns 64 s ..
+// 64 s + 63) into A resp. B slot `slot`; issue_a issues all A loads of a stage,
+// issue_b_part a quarter of the B loads.
+__device__ __forceinline__ void load16_lds(__amdgpu_buffer_rsrc_t r, bf16_t* lds, int voff, int soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds, 16, voff, soff, 0, 0);
+}
+template <class C>
+__device__ __forceinline__ void load_a(const KLoop& L, int s, int slot, int j) {
+  load16_lds(L.ra, L.smem + slot * C::A_ELEMS + L.lds_a_load + j * 8 * BK, L.a_lane[j & 1],
+             (L.a_row0 + 8 * j) * L.row_bytes + s * BK * 2);
+}
+template <class C>
+__device__ __forceinline__ void load_b(const KLoop& L, int s, int slot, int j) {
+  load16_lds(L.rb, L.smem + C::B_RING + slot * C::B_ELEMS + L.lds_b_load + j * 8 * BK, L.b_lane[j & 1],
+             L.b_row[j] * L.row_bytes + s * BK * 2);
+}
 template <class C>
 __device__ __forceinline__ void issue_a(const KLoop& L, int s, int slot) {
-  bf16_t* d = L.smem + slot * C::A_ELEMS + L.lds_a_load;
-  const int ko = s * BK * 2;
 #pragma unroll
-  for (int j = 0; j < C::A_LOADS; ++j)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(L.ra, d + j * 8 * BK, 16, L.a_lane[j & 1],
-                                             (L.a_row0 + 8 * j) * L.row_bytes + ko, 0, 0);
+  for (int j = 0; j < C::A_LOADS; ++j) load_a<C>(L, s, slot, j);
 }
 // Part q (q < BK/16) of the B loads of stage s: loads j = q*kBPart .. +kBPart-1.
 template <class C>
 __device__ __forceinline__ void issue_b_part(const KLoop& L, int s, int slot, int q) {
-  bf16_t* d = L.smem + C::B_RING + slot * C::B_ELEMS + L.lds_b_load;
 #pragma unroll
-  for (int i = 0; i < kBPart; ++i) {
-    const int j = q * kBPart + i;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(L.rb, d + j * 8 * BK, 16, L.b_lane[j & 1],
-                                             L.b_row[j] * L.row_bytes + s * BK * 2, 0, 0);
-  }
+  for (int i = 0; i < kBPart; ++i) load_b<C>(L, s, slot, q * kBPart + i);
 }
 template <class C>
 __device__ __forceinline__ void issue_b(const KLoop& L, int s, int slot) {
@@ -210,40 +215,85 @@ struct LoadOrder {
 // wn*TN + nb*32 + lrow; (row >> 1) & 7 = (lrow >> 1) & 7 for all of them, so
 // one chunk term per k-step serves every block and the block offsets are
 // immediates.
+template <class C>
+__device__ __forceinline__ const bf16_t* frag_base_a(const KLoop& L, int slot, int ks) {
+  return L.smem + slot * C::A_ELEMS + ((ks * 2 + L.khalf) ^ L.sw) * 8 + L.lds_a;
+}
+template <class C>
+__device__ __forceinline__ const bf16_t* frag_base_b(const KLoop& L, int slot, int ks) {
+  return L.smem + C::B_RING + slot * C::B_ELEMS + ((ks * 2 + L.khalf) ^ L.sw) * 8 + L.lds_b;
+}
 template <class C, int NACT>
 __device__ __forceinline__ void read_frags(const KLoop& L, int slot_a, int slot_b, int ks, Frags<C>& f) {
-  const int chunk = ((ks * 2 + L.khalf) ^ L.sw) * 8;
-  const bf16_t* ba = L.smem + slot_a * C::A_ELEMS + chunk;
-  const bf16_t* bb = L.smem + C::B_RING + slot_b * C::B_ELEMS + chunk;
-  // issued in the order the next k-step's MFMAs (mb-major) consume them
+  const bf16_t* ba = frag_base_a<C>(L, slot_a, ks);
+  const bf16_t* bb = frag_base_b<C>(L, slot_b, ks);
 #pragma unroll
-  for (int nb = 0; nb < C::NB; ++nb)
-    f.b[nb] = *reinterpret_cast<const bf16x8*>(bb + L.lds_b + nb * 32 * BK);
+  for (int nb = 0; nb < C::NB; ++nb) f.b[nb] = *reinterpret_cast<const bf16x8*>(bb + nb * 32 * BK);
 #pragma unroll
-  for (int mb = 0; mb < NACT; ++mb)
-    f.a[mb] = *reinterpret_cast<const bf16x8*>(ba + L.lds_a + mb * 32 * BK);
+  for (int mb = 0; mb < NACT; ++mb) f.a[mb] = *reinterpret_cast<const bf16x8*>(ba + mb * 32 * BK);
 }
 
-template <class C, int NACT>
-__device__ __forceinline__ void mfmas(const Frags<C>& f, floatx16 (&acc)[C::MB][C::NB]) {
-#pragma unroll
-  for (int mb = 0; mb < NACT; ++mb)
-#pragma unroll
-    for (int nb = 0; nb < C::NB; ++nb)
-      acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[mb], f.b[nb], acc[mb][nb], 0, 0, 0);
+// Buffer loads placed in one k-step: the first NA are A loads 0..NA-1 of
+// stage a_s into A slot a_slot, the rest B loads b_j0, b_j0+1, ... of stage
+// b_s into B slot b_slot.
+struct StepLoads {
+  int a_s, a_slot, b_s, b_slot, b_j0;
+};
+template <class C, int NA>
+__device__ __forceinline__ void step_load(const KLoop& L, const StepLoads& ld, int j) {
+  if (j < NA) load_a<C>(L, ld.a_s, ld.a_slot, j);
+  else load_b<C>(L, ld.b_s, ld.b_slot, ld.b_j0 + j - NA);
 }
 
-// Scheduling groups for one k-step: M MFMAs with R fragment reads and V
-// buffer loads spread evenly between them.
-template <int R, int M, int V, int I = 0>
-__device__ __forceinline__ void interleave3() {
-  if constexpr (I < M) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
-    constexpr int r = ((I + 1) * R) / M - (I * R) / M;
-    if constexpr (r > 0) __builtin_amdgcn_sched_group_barrier(0x100, r, 0);  // DS reads
-    constexpr int v = ((I + 1) * V) / M - (I * V) / M;
-    if constexpr (v > 0) __builtin_amdgcn_sched_group_barrier(0x020, v, 0);  // VMEM reads
-    interleave3<R, M, V, I + 1>();
+// One k-step in a fixed issue order.  Its MFMAs run block row by block row
+// (mb-major); the other work goes between them: first the fragment reads of
+// the next k-step, B blocks then A blocks (the order in which that k-step's
+// MFMAs consume them), then the V buffer loads of `ld`.  Op j of
+// those R + V goes right after MFMA (j M) / (R + V), so every fragment is
+// read at least M - R MFMAs before its first use and no wave issues a burst
+// of loads.  Scheduling barriers fence each instruction group: the machine
+// scheduler would otherwise move reads next to their consumers, which
+// exposes the LDS latency.
+// TR: the MFMA takes the weight fragment as its first operand, so the 32 x 32
+// accumulator block is (weight row, token row): lane l holds token row
+// l % 32 and weight rows 8 (v / 4) + 4 (l / 32) + v % 4, four consecutive
+// output columns per group of four registers.  Otherwise the block is
+// (token row, weight row): lane l holds output column l % 32 of token rows
+// 8 (v / 4) + 4 (l / 32) + v % 4.  Either way every output is the same chain
+// of MFMAs over K.
+template <class C, int NACT, int NA, int V, bool TR>
+__device__ __forceinline__ void kstep(const KLoop& L, const Frags<C>& cur, Frags<C>& nxt, int slot_a, int slot_b,
+                                      int ks_next, floatx16 (&acc)[C::MB][C::NB], const StepLoads& ld) {
+  constexpr int M = NACT * C::NB;
+  constexpr int R = NACT > 0 ? C::NB + NACT : 0;
+  constexpr int OPS = R + V;
+  if constexpr (M == 0) {
+#pragma unroll
+    for (int j = 0; j < V; ++j) step_load<C, NA>(L, ld, j);
+  } else {
+    const bf16_t* ba = frag_base_a<C>(L, slot_a, ks_next);
+    const bf16_t* bb = frag_base_b<C>(L, slot_b, ks_next);
+#pragma unroll
+    for (int i = 0; i < M; ++i) {
+      const int mb = i / C::NB, nb = i % C::NB;
+      if constexpr (TR)
+        acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur.b[nb], cur.a[mb], acc[mb][nb], 0, 0, 0);
+      else
+        acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur.a[mb], cur.b[nb], acc[mb][nb], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int j = 0; j < OPS; ++j) {
+        if ((j * M) / OPS == i) {
+          if (j < C::NB)
+            nxt.b[j] = *reinterpret_cast<const bf16x8*>(bb + j * 32 * BK);
+          else if (j < R)
+            nxt.a[j - C::NB] = *reinterpret_cast<const bf16x8*>(ba + (j - C::NB) * 32 * BK);
+          else
+            step_load<C, NA>(L, ld, j - R);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+    }
   }
 }
 
@@ -255,7 +305,7 @@ __device__ __forceinline__ void interleave3() {
 // B(kt+SB) are issued into them (see the load order above) and the first
 // fragments of stage kt+1 are read.  NACT = active 32-row blocks of the wave's
 // rows (inactive blocks of a ragged tile get neither LDS reads nor MFMAs).
-template <class C, int NACT>
+template <class C, int NACT, bool TR>
 __device__ __forceinline__ void k_loop(const KLoop& L, floatx16 (&acc)[C::MB][C::NB]) {
   const int nk = L.nk, last = nk - 1;
 #pragma unroll
@@ -277,31 +327,19 @@ __device__ __forceinline__ void k_loop(const KLoop& L, floatx16 (&acc)[C::MB][C:
   for (int kt = 0; kt < nk; ++kt) {
 #pragma unroll
     for (int ks = 0; ks < kKsteps - 1; ++ks) {
-      issue_b_part<C>(L, pb_s, pb_slot, ks + 1);
-      if (NACT > 0) {
-        read_frags<C, NACT>(L, ca, cb, ks + 1, f[(ks + 1) & 1]);
-        mfmas<C, NACT>(f[ks & 1], acc);
-        // keep the next k-step's fragment reads and the loads spread between
-        // this k-step's MFMAs (the machine scheduler would otherwise move
-        // reads next to their consumers and expose LDS latency)
-        interleave3<NACT + C::NB, NACT * C::NB, kBPart>();
-      }
+      const StepLoads ld{0, 0, pb_s, pb_slot, (ks + 1) * kBPart};
+      kstep<C, NACT, 0, kBPart, TR>(L, f[ks & 1], f[(ks + 1) & 1], ca, cb, ks + 1, acc, ld);
     }
     // every fragment of stage kt is in registers, stage kt+1 has landed
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
     wait_vm<LoadOrder<C>::after_next()>();
     bar();
-    issue_a<C>(L, min(kt + C::SA, last), ca);
     pb_s = min(kt + C::SB, last);
     pb_slot = cb;
-    issue_b_part<C>(L, pb_s, pb_slot, 0);
+    const StepLoads ld{min(kt + C::SA, last), ca, pb_s, pb_slot, 0};
     const int na = ca + 1 == C::SA ? 0 : ca + 1;
     const int nb = cb + 1 == C::SB ? 0 : cb + 1;
-    if (NACT > 0) {
-      read_frags<C, NACT>(L, na, nb, 0, f[0]);
-      mfmas<C, NACT>(f[(kKsteps - 1) & 1], acc);
-      interleave3<NACT + C::NB, NACT * C::NB, C::A_LOADS + kBPart>();
-    }
+    kstep<C, NACT, C::A_LOADS, C::A_LOADS + kBPart, TR>(L, f[(kKsteps - 1) & 1], f[0], na, nb, 0, acc, ld);
     ca = na;
     cb = nb;
   }
@@ -371,53 +409,76 @@ __device__ __forceinline__ void run_item(const GroupedProblem& p, bf16_t* smem, 
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
+  // the gate/up accumulators are transposed (8-byte bf16 stores of four
+  // consecutive f); the down GEMM's are not (whole 128-byte lines of fp32
+  // partial sums or 64-byte runs of bf16 per store)
+  constexpr bool TR = MODE == MODE_GATEUP;
   // 32-row blocks of this wave's TM rows that hold rows of the group
   const int nact = min(C::MB, max(0, (row_end - (row0 + wm * C::TM) + 31) / 32));
   if constexpr (C::MB == 4) {
     switch (nact) {
-      case 4: k_loop<C, 4>(kl, acc); break;
-      case 3: k_loop<C, 3>(kl, acc); break;
-      case 2: k_loop<C, 2>(kl, acc); break;
-      case 1: k_loop<C, 1>(kl, acc); break;
-      default: k_loop<C, 0>(kl, acc); break;
+      case 4: k_loop<C, 4, TR>(kl, acc); break;
+      case 3: k_loop<C, 3, TR>(kl, acc); break;
+      case 2: k_loop<C, 2, TR>(kl, acc); break;
+      case 1: k_loop<C, 1, TR>(kl, acc); break;
+      default: k_loop<C, 0, TR>(kl, acc); break;
     }
   } else if constexpr (C::MB == 2) {
     switch (nact) {
-      case 2: k_loop<C, 2>(kl, acc); break;
-      case 1: k_loop<C, 1>(kl, acc); break;
-      default: k_loop<C, 0>(kl, acc); break;
+      case 2: k_loop<C, 2, TR>(kl, acc); break;
+      case 1: k_loop<C, 1, TR>(kl, acc); break;
+      default: k_loop<C, 0, TR>(kl, acc); break;
     }
   } else {
     static_assert(C::MB == 1, "tile shape");
-    if (nact == 1) k_loop<C, 1>(kl, acc); else k_loop<C, 0>(kl, acc);
+    if (nact == 1) k_loop<C, 1, TR>(kl, acc); else k_loop<C, 0, TR>(kl, acc);
   }
   __syncthreads();  // every wave is done with the ring before the next item refills it
 
-  // epilogue: acc[mb][nb][v] is C[row][col] with col = lane%32 of the 32x32
-  // block and row = 8*(v/4) + 4*(lane/32) + v%4
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  // float pair to packed bf16, round to nearest even (one hardware conversion)
+  auto pack2 = [](float a, float b) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){a, b}, bf16x2));
+  };
+  if constexpr (MODE == MODE_GATEUP) {
+    // acc[mb][nb][4 g + q]: token row wm*TM + mb*32 + lrow, weight row
+    // wn*TN + nb*32 + 8 g + 4 khalf + q; blocks nb < NB/2 are gate rows and
+    // nb + NB/2 the up rows of the same f, so four consecutive f per g
 #pragma unroll
-  for (int mb = 0; mb < C::MB; ++mb) {
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int row = row0 + wm * C::TM + mb * 32 + 8 * (v >> 2) + 4 * khalf + (v & 3);
+    for (int mb = 0; mb < C::MB; ++mb) {
+      const int row = row0 + wm * C::TM + mb * 32 + lrow;
       if (row >= row_end) continue;
-      if (MODE == MODE_GATEUP) {
 #pragma unroll
-        for (int nb = 0; nb < C::NB / 2; ++nb) {
-          const int f = ni * (BN / 2) + wn * (C::TN / 2) + nb * 32 + lrow;
-          C_out[(size_t)row * p.F + f] = f32_to_bf16(swiglu(acc[mb][nb][v], acc[mb][nb + C::NB / 2][v]));
+      for (int nb = 0; nb < C::NB / 2; ++nb) {
+        const floatx16& gt = acc[mb][nb];
+        const floatx16& up = acc[mb][nb + C::NB / 2];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int f = ni * (BN / 2) + wn * (C::TN / 2) + nb * 32 + 8 * g + 4 * khalf;
+          uint2 v;
+          v.x = pack2(swiglu(gt[4 * g], up[4 * g]), swiglu(gt[4 * g + 1], up[4 * g + 1]));
+          v.y = pack2(swiglu(gt[4 * g + 2], up[4 * g + 2]), swiglu(gt[4 * g + 3], up[4 * g + 3]));
+          *reinterpret_cast<uint2*>(C_out + (size_t)row * p.F + f) = v;
         }
-      } else if (part != nullptr) {
+      }
+    }
+  } else {
+    // acc[mb][nb][v]: output column wn*TN + nb*32 + lrow of token row
+    // wm*TM + mb*32 + 8 (v / 4) + 4 khalf + v % 4
+#pragma unroll
+    for (int mb = 0; mb < C::MB; ++mb) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = row0 + wm * C::TM + mb * 32 + 8 * (v >> 2) + 4 * khalf + (v & 3);
+        if (row >= row_end) continue;
 #pragma unroll
         for (int nb = 0; nb < C::NB; ++nb) {
           const int n = ni * BN + wn * C::TN + nb * 32 + lrow;
-          part[(size_t)row * p.H + n] = acc[mb][nb][v];
-        }
-      } else {
-#pragma unroll
-        for (int nb = 0; nb < C::NB; ++nb) {
-          const int n = ni * BN + wn * C::TN + nb * 32 + lrow;
-          C_out[(size_t)row * p.H + n] = f32_to_bf16(acc[mb][nb][v]);
+          if (part != nullptr)
+            part[(size_t)row * p.H + n] = acc[mb][nb][v];
+          else
+            C_out[(size_t)row * p.H + n] = (bf16_t)(pack2(acc[mb][nb][v], 0.f) & 0xffffu);
         }
       }
     }
