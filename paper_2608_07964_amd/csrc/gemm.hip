@@ -359,6 +359,11 @@ __device__ __forceinline__ void run_item(const GroupedProblem& p, bf16_t* smem, 
                                          int lane) {
   const int wm = wave / C::WN, wn = wave % C::WN;
   const int lrow = lane & 31, khalf = lane >> 5;
+  // rows per wavefront row: the tile's rows split evenly over the WM
+  // wavefront rows in whole 32-row blocks (a 150-row tile gives each of two
+  // wavefront rows 96 rows, 3 blocks, instead of 128 + 22); the slowest
+  // wavefront row sets the item's time
+  const int tm = min(C::TM, 32 * ((row_end - row0 + 32 * C::WM - 1) / (32 * C::WM)));
   const int lr = lane >> 3, lp = lane & 7;
   const int k_off = ks0 * BK;  // first K column of the item
   const bf16_t* Atile = A + (size_t)row0 * K + k_off;
@@ -395,7 +400,7 @@ __device__ __forceinline__ void run_item(const GroupedProblem& p, bf16_t* smem, 
   }
   kl.lds_a_load = (C::BM / kWaves) * wave * BK;
   kl.lds_b_load = (BN / kWaves) * wave * BK;
-  kl.lds_a = (wm * C::TM + lrow) * BK;
+  kl.lds_a = (wm * tm + lrow) * BK;
   kl.lds_b = (wn * C::TN + lrow) * BK;
   kl.sw = (lrow >> 1) & 7;
   kl.nk = nks;
@@ -414,7 +419,7 @@ __device__ __forceinline__ void run_item(const GroupedProblem& p, bf16_t* smem, 
   // partial sums or 64-byte runs of bf16 per store)
   constexpr bool TR = MODE == MODE_GATEUP;
   // 32-row blocks of this wave's TM rows that hold rows of the group
-  const int nact = min(C::MB, max(0, (row_end - (row0 + wm * C::TM) + 31) / 32));
+  const int nact = min(tm / 32, max(0, (row_end - (row0 + wm * tm) + 31) / 32));
   if constexpr (C::MB == 4) {
     switch (nact) {
       case 4: k_loop<C, 4, TR>(kl, acc); break;
@@ -447,8 +452,10 @@ __device__ __forceinline__ void run_item(const GroupedProblem& p, bf16_t* smem, 
     // nb + NB/2 the up rows of the same f, so four consecutive f per g
 #pragma unroll
     for (int mb = 0; mb < C::MB; ++mb) {
-      const int row = row0 + wm * C::TM + mb * 32 + lrow;
-      if (row >= row_end) continue;
+      // blocks past nact were not computed (and may be another wavefront
+      // row's rows)
+      const int row = row0 + wm * tm + mb * 32 + lrow;
+      if (mb >= nact || row >= row_end) continue;
 #pragma unroll
       for (int nb = 0; nb < C::NB / 2; ++nb) {
         const floatx16& gt = acc[mb][nb];
@@ -468,9 +475,10 @@ __device__ __forceinline__ void run_item(const GroupedProblem& p, bf16_t* smem, 
     // wm*TM + mb*32 + 8 (v / 4) + 4 khalf + v % 4
 #pragma unroll
     for (int mb = 0; mb < C::MB; ++mb) {
+      if (mb >= nact) continue;
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const int row = row0 + wm * C::TM + mb * 32 + 8 * (v >> 2) + 4 * khalf + (v & 3);
+        const int row = row0 + wm * tm + mb * 32 + 8 * (v >> 2) + 4 * khalf + (v & 3);
         if (row >= row_end) continue;
 #pragma unroll
         for (int nb = 0; nb < C::NB; ++nb) {

@@ -215,3 +215,63 @@ def test_schedule_invariance_and_replay(cfg, device):
     eb = results[("maxutil", cfg.m)][1]
     assert (ometrics.utilization(loads_ls, [s.runset for s in eb])
             >= ometrics.utilization(loads_ls, osched.separate_steps(cfg.N, cfg.L)))
+
+
+# group sizes on both sides of every tile-shape boundary (64 / 128 / 256-row
+# m-tiles, 32-row MFMA blocks, rows split evenly over two wavefront rows)
+EDGE_SIZES = [[150, 129, 193, 65, 33, 1, 287, 64], [160, 161, 192, 128, 127, 63, 31, 256],
+              [255, 257, 96, 32, 0, 97, 200, 3]]
+
+
+def test_moe_step_group_sizes_span_tile_shapes(device):
+    """Crafted routing (not the router's): three entries at different layers
+    whose (layer, expert) groups take every row count around the tile-shape
+    boundaries; every row of h and o checked against the oracle."""
+    B = _binding()
+    cfg = mini(CONFIGS[1], H=256, F=256, L=3)
+    assert cfg.k == 2 and cfg.E == 8 and cfg.S == 0
+    log(f"group-size parity {cfg.name}")
+    inp = DeviceInputs(cfg, device)
+    P = host_weights(cfg)
+    cast = cast_fn(cfg.dtype)
+    desc = B.make_desc(cfg.L, cfg.H, cfg.F, cfg.E, cfg.k, cfg.S, cfg.D, cfg.dtype, cfg.eps)
+    ents = []
+    for l, sizes in enumerate(EDGE_SIZES):
+        T = sum(sizes) // 2
+        assert sum(sizes) == 2 * T and max(sizes) <= T
+        # slot 0 takes the first T ids of the sorted list, slot 1 the rest: a
+        # token's two experts differ because no expert has more than T pairs
+        ids = np.repeat(np.arange(cfg.E), sizes).astype(np.int32)
+        idx = np.stack([ids[:T], ids[T:]], axis=1)
+        assert (idx[:, 0] != idx[:, 1]).all()
+        a = fill_(torch.empty(T, cfg.H, dtype=torch.bfloat16, device=device), cfg, gen.KIND_X, l)
+        ents.append(dict(j=l, l=l, T=T, a=a, idx=torch.from_numpy(idx).to(device),
+                         w=torch.full((T, 2), 0.5, device=device), idx_np=idx))
+    run = B.work_array((e["j"], e["l"], e["T"], e["a"], e["idx"], e["w"]) for e in ents)
+    Ts = [e["T"] for e in ents]
+    Ptot = 2 * sum(Ts)
+    ws_bytes = B.easybalance_moe_step_workspace_size(desc, Ts)
+    ws = torch.empty(ws_bytes + 256, dtype=torch.uint8, device=device)
+    wsp = ws.data_ptr() + (-ws.data_ptr()) % 256
+    o = torch.empty(Ptot, cfg.H, dtype=torch.bfloat16, device=device)
+    inv = torch.empty(Ptot, dtype=torch.int32, device=device)
+    views = dict(a_perm=torch.empty(Ptot, cfg.H, dtype=torch.bfloat16, device=device),
+                 h=torch.empty(Ptot, cfg.F, dtype=torch.bfloat16, device=device),
+                 perm=torch.empty(Ptot, dtype=torch.int32, device=device),
+                 offsets=torch.empty(cfg.L * cfg.E + 1, dtype=torch.int32, device=device))
+    B.easybalance_moe_step(desc, run, len(ents), inp.W_gu, inp.W_dn, wsp, ws_bytes, o, inv, views)
+    torch.cuda.synchronize()
+    off = views["offsets"].cpu().numpy()
+    got_sizes = np.diff(off).reshape(cfg.L, cfg.E)
+    assert np.array_equal(got_sizes, np.asarray(EDGE_SIZES))
+    a_perm, h_gpu, o_gpu = to_np(views["a_perm"]), to_np(views["h"]), to_np(o)
+    for key in range(cfg.L * cfg.E):
+        r0, r1 = off[key], off[key + 1]
+        if r0 == r1:
+            continue
+        l, e = divmod(key, cfg.E)
+        Wg_, Wu_ = P.gate_up(l, e)
+        h_ref, _ = omodel.expert_ffn(a_perm[r0:r1], Wg_, Wu_, P.down(l, e), cast)
+        assert_close(h_gpu[r0:r1], h_ref, cfg.dtype, f"h rows={r1 - r0}")
+        o_ref = cast(h_gpu[r0:r1] @ np.asarray(P.down(l, e), np.float64).T)
+        assert_close(o_gpu[r0:r1], o_ref, cfg.dtype, f"o rows={r1 - r0}")
