@@ -81,7 +81,7 @@ WsLayout ws_layout(const eb_model_desc& d, const StepShape& s, const eb_step_vie
   w.hist = take(sizeof(int32_t) * (size_t)s.n_chunks * d.E);
   w.chunk_base = take(sizeof(int32_t) * (size_t)s.n_chunks * (d.E + d.S));
   w.offsets = (v && v->offsets) ? 0 : take(sizeof(int32_t) * ((size_t)d.L * (d.E + d.S) + 1));
-  w.tiles = take(sizeof(int2) * (size_t)(s.max_tiles > 0 ? s.max_tiles : 1));
+  w.tiles = take(sizeof(int4) * (size_t)(s.max_tiles > 0 ? s.max_tiles : 1));
   w.n_tiles = take(sizeof(int32_t));
   w.groups = take(sizeof(int4) * (size_t)d.L * (d.E + d.S));
   w.n_groups = take(sizeof(int32_t));
@@ -282,7 +282,7 @@ int easybalance_moe_step(const eb_model_desc* desc, int32_t n_run, const eb_work
   int32_t* hist = reinterpret_cast<int32_t*>(base + L.hist);
   int32_t* chunk_base = reinterpret_cast<int32_t*>(base + L.chunk_base);
   int32_t* offsets = (views && views->offsets) ? views->offsets : reinterpret_cast<int32_t*>(base + L.offsets);
-  int2* tiles = reinterpret_cast<int2*>(base + L.tiles);
+  int4* tiles = reinterpret_cast<int4*>(base + L.tiles);
   int32_t* n_tiles = reinterpret_cast<int32_t*>(base + L.n_tiles);
   int4* groups = reinterpret_cast<int4*>(base + L.groups);
   int32_t* n_groups = reinterpret_cast<int32_t*>(base + L.n_groups);

@@ -36,7 +36,8 @@ struct GroupedProblem {
   int32_t H, F, E, S;                      // E+S expert slots per layer
   int32_t P;                               // grouped rows
   const int32_t* offsets;                  // [L*(E+S)+1]
-  const int2* tiles;                       // [n_tiles] (key, first row)
+  const int4* tiles;                       // [n_tiles] the row block's group: (key, first row,
+                                           // rows, index of the group's first row block)
   const int32_t* n_tiles;                  // device scalar: row blocks over all groups
   const int4* groups;                      // [n_groups] (key, first row, rows, first row block)
   const int32_t* n_groups;                 // device scalar: non-empty keys
@@ -92,7 +93,7 @@ hipError_t launch_route(const eb_model_desc& d, int T, const float* x, const flo
 
 hipError_t launch_perm_count(const RunTable& rt, int n_chunks, int32_t* hist, hipStream_t s);
 hipError_t launch_perm_scan(const RunTable& rt, int n_chunks, const int32_t* hist,
-                            int32_t* chunk_base, int32_t* offsets, int2* tiles,
+                            int32_t* chunk_base, int32_t* offsets, int4* tiles,
                             int32_t* n_tiles, int4* groups, int32_t* n_groups, int bm,
                             int max_tiles, int32_t* work_ctr, hipStream_t s);
 hipError_t launch_perm_scatter(const RunTable& rt, int n_chunks, int P, int elem_bytes,

@@ -2,7 +2,7 @@
 // from whatever layer, in one launch per GEMM (cross-layer workload
 // combination, Section 4.1).  Groups are the contiguous row ranges
 // offsets[key] .. offsets[key+1] of the grouped activations; the tile list
-// (key, first row) comes from the permutation scan.
+// (the group record of every row block) comes from the permutation scan.
 //
 //   gate/up:  h = dtype( SiLU(A Wgate^T) * (A Wup^T) )   A [P][H], W_gu[l][e] [2F][H]
 //   down:     o = dtype( h Wdown^T )                     h [P][F], W_dn[l][e] [H][F]
@@ -348,6 +348,82 @@ __device__ __forceinline__ void k_loop(const KLoop& L, floatx16 (&acc)[C::MB][C:
   wait_vm<0>();
 }
 
+// K loop of the wave's nact active 32-row blocks (a compile-time count).
+template <class C, bool TR>
+__device__ __forceinline__ void k_loop_nact(const KLoop& kl, floatx16 (&acc)[C::MB][C::NB], int nact) {
+  if constexpr (C::MB == 4) {
+    switch (nact) {
+      case 4: k_loop<C, 4, TR>(kl, acc); break;
+      case 3: k_loop<C, 3, TR>(kl, acc); break;
+      case 2: k_loop<C, 2, TR>(kl, acc); break;
+      case 1: k_loop<C, 1, TR>(kl, acc); break;
+      default: k_loop<C, 0, TR>(kl, acc); break;
+    }
+  } else if constexpr (C::MB == 2) {
+    switch (nact) {
+      case 2: k_loop<C, 2, TR>(kl, acc); break;
+      case 1: k_loop<C, 1, TR>(kl, acc); break;
+      default: k_loop<C, 0, TR>(kl, acc); break;
+    }
+  } else {
+    static_assert(C::MB == 1, "tile shape");
+    if (nact == 1) k_loop<C, 1, TR>(kl, acc); else k_loop<C, 0, TR>(kl, acc);
+  }
+}
+
+// Float pair to packed bf16, round to nearest even (one hardware conversion).
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){a, b}, bf16x2));
+}
+
+// bf16 epilogue of transposed accumulators: acc[mb][nb][4 g + q] is token
+// row r0w + mb*32 + lrow (r0w = the wavefront row's first row in the tile)
+// and weight row wn*TN + nb*32 + 8 g + 4 khalf + q, i.e. four consecutive
+// output columns per g.  Gate/up: blocks nb < NB/2 are gate rows and
+// nb + NB/2 the up rows of the same f; h = bf16(SwiGLU(gate, up)).  Down:
+// o = bf16(acc).  Blocks past nact were not computed (and may be another
+// wavefront row's rows).
+template <class C, int MODE>
+__device__ __forceinline__ void epilogue_tr(const GroupedProblem& p, const floatx16 (&acc)[C::MB][C::NB],
+                                            bf16_t* C_out, int row0, int row_end, int ni, int r0w, int wn,
+                                            int nact, int lrow, int khalf) {
+#pragma unroll
+  for (int mb = 0; mb < C::MB; ++mb) {
+    const int row = row0 + r0w + mb * 32 + lrow;
+    if (mb >= nact || row >= row_end) continue;
+    if constexpr (MODE == MODE_GATEUP) {
+#pragma unroll
+      for (int nb = 0; nb < C::NB / 2; ++nb) {
+        const floatx16& gt = acc[mb][nb];
+        const floatx16& up = acc[mb][nb + C::NB / 2];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int f = ni * (BN / 2) + wn * (C::TN / 2) + nb * 32 + 8 * g + 4 * khalf;
+          uint2 v;
+          v.x = pack_bf16x2(swiglu(gt[4 * g], up[4 * g]), swiglu(gt[4 * g + 1], up[4 * g + 1]));
+          v.y = pack_bf16x2(swiglu(gt[4 * g + 2], up[4 * g + 2]), swiglu(gt[4 * g + 3], up[4 * g + 3]));
+          *reinterpret_cast<uint2*>(C_out + (size_t)row * p.F + f) = v;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int nb = 0; nb < C::NB; ++nb) {
+        const floatx16& c = acc[mb][nb];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int n = ni * BN + wn * C::TN + nb * 32 + 8 * g + 4 * khalf;
+          uint2 v;
+          v.x = pack_bf16x2(c[4 * g], c[4 * g + 1]);
+          v.y = pack_bf16x2(c[4 * g + 2], c[4 * g + 3]);
+          *reinterpret_cast<uint2*>(C_out + (size_t)row * p.H + n) = v;
+        }
+      }
+    }
+  }
+}
+
 // One work item (m-tile row0.. of group rows ending at row_end, n-tile ni,
 // K stages ks0 .. ks0+nks-1) in tile shape C.  part == nullptr: the item
 // covers all of K and writes the output; else it writes its fp32 partial
@@ -414,65 +490,20 @@ __device__ __forceinline__ void run_item(const GroupedProblem& p, bf16_t* smem, 
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  // the gate/up accumulators are transposed (8-byte bf16 stores of four
-  // consecutive f); the down GEMM's are not (whole 128-byte lines of fp32
-  // partial sums or 64-byte runs of bf16 per store)
-  constexpr bool TR = MODE == MODE_GATEUP;
   // 32-row blocks of this wave's TM rows that hold rows of the group
   const int nact = min(tm / 32, max(0, (row_end - (row0 + wm * tm) + 31) / 32));
-  if constexpr (C::MB == 4) {
-    switch (nact) {
-      case 4: k_loop<C, 4, TR>(kl, acc); break;
-      case 3: k_loop<C, 3, TR>(kl, acc); break;
-      case 2: k_loop<C, 2, TR>(kl, acc); break;
-      case 1: k_loop<C, 1, TR>(kl, acc); break;
-      default: k_loop<C, 0, TR>(kl, acc); break;
-    }
-  } else if constexpr (C::MB == 2) {
-    switch (nact) {
-      case 2: k_loop<C, 2, TR>(kl, acc); break;
-      case 1: k_loop<C, 1, TR>(kl, acc); break;
-      default: k_loop<C, 0, TR>(kl, acc); break;
-    }
-  } else {
-    static_assert(C::MB == 1, "tile shape");
-    if (nact == 1) k_loop<C, 1, TR>(kl, acc); else k_loop<C, 0, TR>(kl, acc);
-  }
-  __syncthreads();  // every wave is done with the ring before the next item refills it
-
-  typedef float f32x2 __attribute__((ext_vector_type(2)));
-  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-  // float pair to packed bf16, round to nearest even (one hardware conversion)
-  auto pack2 = [](float a, float b) {
-    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){a, b}, bf16x2));
-  };
-  if constexpr (MODE == MODE_GATEUP) {
-    // acc[mb][nb][4 g + q]: token row wm*TM + mb*32 + lrow, weight row
-    // wn*TN + nb*32 + 8 g + 4 khalf + q; blocks nb < NB/2 are gate rows and
-    // nb + NB/2 the up rows of the same f, so four consecutive f per g
-#pragma unroll
-    for (int mb = 0; mb < C::MB; ++mb) {
-      // blocks past nact were not computed (and may be another wavefront
-      // row's rows)
-      const int row = row0 + wm * tm + mb * 32 + lrow;
-      if (mb >= nact || row >= row_end) continue;
-#pragma unroll
-      for (int nb = 0; nb < C::NB / 2; ++nb) {
-        const floatx16& gt = acc[mb][nb];
-        const floatx16& up = acc[mb][nb + C::NB / 2];
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int f = ni * (BN / 2) + wn * (C::TN / 2) + nb * 32 + 8 * g + 4 * khalf;
-          uint2 v;
-          v.x = pack2(swiglu(gt[4 * g], up[4 * g]), swiglu(gt[4 * g + 1], up[4 * g + 1]));
-          v.y = pack2(swiglu(gt[4 * g + 2], up[4 * g + 2]), swiglu(gt[4 * g + 3], up[4 * g + 3]));
-          *reinterpret_cast<uint2*>(C_out + (size_t)row * p.F + f) = v;
-        }
-      }
-    }
-  } else {
+  // bf16 outputs use the transposed accumulators (one 8-byte store per four
+  // consecutive columns); fp32 partial sums the row layout (32 lanes store a
+  // whole 128-byte line)
+  if (MODE == MODE_GATEUP || part == nullptr) {
+    k_loop_nact<C, true>(kl, acc, nact);
+    __syncthreads();  // every wave is done with the ring before the next item refills it
+    epilogue_tr<C, MODE>(p, acc, C_out, row0, row_end, ni, wm * tm, wn, nact, lrow, khalf);
+  } else if constexpr (MODE == MODE_DOWN) {
+    k_loop_nact<C, false>(kl, acc, nact);
+    __syncthreads();
     // acc[mb][nb][v]: output column wn*TN + nb*32 + lrow of token row
-    // wm*TM + mb*32 + 8 (v / 4) + 4 khalf + v % 4
+    // wm*tm + mb*32 + 8 (v / 4) + 4 khalf + v % 4
 #pragma unroll
     for (int mb = 0; mb < C::MB; ++mb) {
       if (mb >= nact) continue;
@@ -481,13 +512,8 @@ __device__ __forceinline__ void run_item(const GroupedProblem& p, bf16_t* smem, 
         const int row = row0 + wm * tm + mb * 32 + 8 * (v >> 2) + 4 * khalf + (v & 3);
         if (row >= row_end) continue;
 #pragma unroll
-        for (int nb = 0; nb < C::NB; ++nb) {
-          const int n = ni * BN + wn * C::TN + nb * 32 + lrow;
-          if (part != nullptr)
-            part[(size_t)row * p.H + n] = acc[mb][nb][v];
-          else
-            C_out[(size_t)row * p.H + n] = (bf16_t)(pack2(acc[mb][nb][v], 0.f) & 0xffffu);
-        }
+        for (int nb = 0; nb < C::NB; ++nb)
+          part[(size_t)row * p.H + ni * BN + wn * C::TN + nb * 32 + lrow] = acc[mb][nb][v];
       }
     }
   }
@@ -519,7 +545,6 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_bf16(GroupedProblem 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int xcd = blockIdx.x % kXcds;
-  const int G = *p.n_groups;
   const int ksplit = MODE == MODE_DOWN ? p.ksplit : 1;
   const int nsub = n_ntiles * ksplit;  // items per m-tile
   const long long total = (long long)(*p.n_tiles) * nsub;
@@ -546,13 +571,9 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_bf16(GroupedProblem 
   while (it >= 0) {
     int got = 0;
     if (tid == 0) got = atomicAdd(&p.work_ctr[victim], 1);
-    // group of this item: the last g with cum_mt[g] * nsub <= it
-    int glo = 0, ghi = G - 1;
-    while (glo < ghi) {
-      const int mid = (glo + ghi + 1) >> 1;
-      if ((long long)p.groups[mid].w * nsub <= it) glo = mid; else ghi = mid - 1;
-    }
-    const int4 gd = p.groups[glo];  // key, first row, rows, first m-tile
+    // group of this item: a group's items it * nsub .. (it + mt) * nsub - 1
+    // cover its m-tiles it .. it + mt - 1, so item / nsub is one of them
+    const int4 gd = p.tiles[it / nsub];  // key, first row, rows, first m-tile
     const int mt = (gd.z + BM - 1) / BM;
     // within the group: K part slowest, then n-tile, m-tile fastest
     const int local = it - gd.w * nsub;
@@ -592,8 +613,8 @@ __global__ __launch_bounds__(256) void grouped_gemm_f32(GroupedProblem p, Weight
   __shared__ float Bs[FBK][FBN + 4];
   const int tile = blockIdx.x;
   if (tile >= *p.n_tiles) return;
-  const int2 td = p.tiles[tile];
-  const int key = td.x, row0 = td.y;
+  const int4 td = p.tiles[tile];  // the tile's group
+  const int key = td.x, row0 = td.y + (tile - td.w) * FBM;
   const int ES = p.E + p.S;
   const int layer = key / ES, e = key - layer * ES;
   const int row_end = p.offsets[key + 1];

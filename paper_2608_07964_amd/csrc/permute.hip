@@ -6,7 +6,7 @@
 //
 //   perm_count_kernel    per 256-token chunk: routed pairs per expert (LDS atomics)
 //   perm_scan_kernel     one workgroup: per-key totals, offsets, per-chunk bases,
-//                        the GEMM tile list (key, first row) of BM-row blocks and
+//                        the GEMM tile list (each BM-row block's group record) and
 //                        the list of non-empty groups (key, first row, rows,
 //                        index of its first row block); it also clears the
 //                        work counters of the step's grouped GEMM launches
@@ -64,7 +64,7 @@ __device__ int block_exclusive_scan(int v, int* sm, int* total) {
 // offsets: [L*(E+S)+1]; chunk_base: [n_chunks][E+S]; tiles: [max_tiles].
 __global__ __launch_bounds__(kScanThreads) void perm_scan_kernel(
     RunTable rt, int n_chunks, const int32_t* __restrict__ hist, int32_t* __restrict__ chunk_base,
-    int32_t* __restrict__ offsets, int2* __restrict__ tiles, int32_t* __restrict__ n_tiles,
+    int32_t* __restrict__ offsets, int4* __restrict__ tiles, int32_t* __restrict__ n_tiles,
     int4* __restrict__ groups, int32_t* __restrict__ n_groups, int bm, int max_tiles,
     int32_t* __restrict__ work_ctr) {
   extern __shared__ int smem[];  // running[n_keys] | scan[kScanThreads]
@@ -118,9 +118,11 @@ __global__ __launch_bounds__(kScanThreads) void perm_scan_kernel(
   int gb = block_exclusive_scan(local_groups, scan, &groups_total);
   for (int i = k0; i < k1; ++i) {
     const int r0 = offsets[i], M = offsets[i + 1] - r0;
-    if (M > 0) groups[gb++] = make_int4(i, r0, M, tb);
+    if (M == 0) continue;
+    const int4 g = make_int4(i, r0, M, tb);
+    groups[gb++] = g;
     for (int m = 0; m < M; m += bm) {
-      if (tb < max_tiles) tiles[tb] = make_int2(i, r0 + m);
+      if (tb < max_tiles) tiles[tb] = g;
       ++tb;
     }
   }
@@ -210,7 +212,7 @@ hipError_t launch_perm_count(const RunTable& rt, int n_chunks, int32_t* hist, hi
 }
 
 hipError_t launch_perm_scan(const RunTable& rt, int n_chunks, const int32_t* hist,
-                            int32_t* chunk_base, int32_t* offsets, int2* tiles,
+                            int32_t* chunk_base, int32_t* offsets, int4* tiles,
                             int32_t* n_tiles, int4* groups, int32_t* n_groups, int bm,
                             int max_tiles, int32_t* work_ctr, hipStream_t s) {
   const size_t smem = sizeof(int) * ((size_t)rt.L * (rt.E + rt.S) + kScanThreads);
