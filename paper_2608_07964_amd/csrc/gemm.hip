@@ -519,9 +519,12 @@ __device__ __forceinline__ void run_item(const GroupedProblem& p, bf16_t* smem, 
   }
 }
 
-// Persistent grouped GEMM.  Work item = (group, n-tile, m-tile of 256 rows),
-// enumerated group by group, n-tile-major, m-tile fastest, so consecutive
-// items share the weight tile.  Workgroup b runs on XCD b % 8 (round-robin
+// Persistent grouped GEMM.  Work item = (group, n-tile, m-tile); a group of
+// R rows has ceil(R / 256) m-tiles sharing its rows evenly, enumerated group
+// by group, n-tile-major, m-tile fastest, so consecutive items share the
+// weight tile and, running at the same pace, read each weight stage from L2
+// once (unequal m-tiles drift apart and fetch the weights again: 2.2-3.5x
+// the weight bytes for two to three m-tiles).  Workgroup b runs on XCD b % 8 (round-robin
 // dispatch) and takes items from its XCD's contiguous eighth of the list
 // through that XCD's atomic counter, so items running together on one L2
 // share weight and activation tiles and no workgroup idles while its XCD has
@@ -582,7 +585,10 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_bf16(GroupedProblem 
     const int ni = rem / mt, mi = rem - ni * mt;
     const int nks = K / BK / ksplit, ks0 = kh * nks;
     float* part = ksplit > 1 ? p.partial + (size_t)kh * p.P * p.H : nullptr;
-    const int row0 = gd.y + mi * BM, row_end = gd.y + gd.z;
+    // the group's mt m-tiles share its rows evenly (whole 32-row blocks), so
+    // they run at the same pace and meet the same weight stages in L2
+    const int rpt = 32 * ((gd.z + 32 * mt - 1) / (32 * mt));
+    const int row0 = gd.y + mi * rpt, row_end = min(gd.y + gd.z, row0 + rpt);
     const int layer = gd.x / ES, e = gd.x - layer * ES;
     const bf16_t* Bbase = MODE == MODE_GATEUP
         ? static_cast<const bf16_t*>(wt.gu[layer]) + (size_t)e * 2 * p.F * p.H
