@@ -56,7 +56,7 @@ extern "C" {
                                    micro-batch every step (per-layer baseline) */
 
 #define EB_MAX_POOL 64          /* micro-batch ids are 0..63 (one bit each)   */
-#define EB_MAXUTIL_MAX_POOL 20  /* MaxUtil enumerates 2^n subsets             */
+#define EB_MAXUTIL_MAX_POOL 20  /* MaxUtil enumerates up to 2^n subsets       */
 #define EB_MAX_RUN 64
 #define EB_MAX_LAYERS 128
 
@@ -154,7 +154,8 @@ int easybalance_route(const eb_model_desc* desc, int32_t layer, int32_t T, const
  * with W = sum_{i in R} load_i; U = 1 if W is all zero.
  *   EB_POLICY_MAXUTIL (Section 4.2): the R with |R| >= min(m, n_pool) of
  *     highest U; ties -> larger |R| -> lexicographically smallest id list.
- *     n_pool <= EB_MAXUTIL_MAX_POOL.
+ *     n_pool <= EB_MAXUTIL_MAX_POOL.  Cost: one visit per candidate set,
+ *     sum_{j <= n_pool - min(m, n_pool)} C(n_pool, j) of them, O(D) each.
  *   EB_POLICY_CUMUTIL (Section 5.2): scan ids ascending, take the first, add
  *     each next one iff it strictly raises U.
  *   EB_POLICY_DIFFPEAK (Section 5.2): scan ids ascending, take the first, add
