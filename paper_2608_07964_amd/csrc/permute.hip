@@ -43,49 +43,84 @@ __global__ __launch_bounds__(kPermChunk) void perm_count_kernel(RunTable rt, int
   for (int e = threadIdx.x; e < rt.E; e += blockDim.x) hist[(size_t)b * rt.E + e] = cnt[e];
 }
 
-// Block-wide exclusive scan of one value per thread (1024 threads); returns
-// the exclusive prefix, writes the total to *total.
-__device__ int block_exclusive_scan(int v, int* sm, int* total) {
-  const int tid = threadIdx.x;
-  sm[tid] = v;
-  __syncthreads();
-  for (int off = 1; off < kScanThreads; off <<= 1) {
-    const int add = tid >= off ? sm[tid - off] : 0;
-    __syncthreads();
-    sm[tid] += add;
-    __syncthreads();
+constexpr int kScanWaves = kScanThreads / kWave;
+constexpr int kMaxKeys = 15360;      // L * (E + S) limit of the descriptor check
+constexpr int kHistWindow = 16384;   // histogram cells held in LDS at once
+
+// Block-wide exclusive scan of one value per thread (1024 threads): a
+// shuffle scan inside each wavefront, then over the 16 wavefront totals;
+// returns the exclusive prefix and writes the total to *total.
+__device__ int block_exclusive_scan(int v, int* wtot, int* total) {
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  int x = v;
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int y = __shfl_up(x, off, kWave);
+    if (lane >= off) x += y;
   }
-  const int incl = sm[tid];
-  *total = sm[kScanThreads - 1];
+  if (lane == kWave - 1) wtot[wave] = x;
   __syncthreads();
-  return incl - v;
+  if (wave == 0) {
+    int t = lane < kScanWaves ? wtot[lane] : 0;
+#pragma unroll
+    for (int off = 1; off < kScanWaves; off <<= 1) {
+      const int y = __shfl_up(t, off, kWave);
+      if (lane >= off) t += y;
+    }
+    if (lane < kScanWaves) wtot[lane] = t;
+  }
+  __syncthreads();
+  const int before = wave > 0 ? wtot[wave - 1] : 0;
+  *total = wtot[kScanWaves - 1];
+  __syncthreads();  // wtot is reused by the next scan
+  return before + x - v;
 }
 
 // offsets: [L*(E+S)+1]; chunk_base: [n_chunks][E+S]; tiles: [max_tiles].
+// The histogram cells (chunk b, column c) go through LDS in windows of
+// kHistWindow / (E+S) chunks (one window unless the step is very large);
+// every global load of a phase is independent of the others.
 __global__ __launch_bounds__(kScanThreads) void perm_scan_kernel(
     RunTable rt, int n_chunks, const int32_t* __restrict__ hist, int32_t* __restrict__ chunk_base,
     int32_t* __restrict__ offsets, int4* __restrict__ tiles, int32_t* __restrict__ n_tiles,
     int4* __restrict__ groups, int32_t* __restrict__ n_groups, int bm, int max_tiles,
     int32_t* __restrict__ work_ctr) {
-  extern __shared__ int smem[];  // running[n_keys] | scan[kScanThreads]
-  if (threadIdx.x < kWorkCounters) work_ctr[threadIdx.x] = 0;
-  const int ES = rt.E + rt.S;
-  const int n_keys = rt.L * ES;
-  int* running = smem;
-  int* scan = smem + n_keys;
+  __shared__ int running[kMaxKeys];              // per-key totals, then offsets / cursors
+  __shared__ int hl[kHistWindow];                // one window of histogram cells
+  __shared__ int wtot[kScanWaves];
+  __shared__ int s_cb[EB_MAX_RUN + 1], s_tb[EB_MAX_RUN + 1], s_ly[EB_MAX_RUN];
   const int tid = threadIdx.x;
-
-  // 1) per-key totals into running[]
+  if (tid < kWorkCounters) work_ctr[tid] = 0;
+  const int E = rt.E, ES = rt.E + rt.S, n = rt.n;
+  const int n_keys = rt.L * ES;
   for (int i = tid; i < n_keys; i += kScanThreads) running[i] = 0;
+  if (tid <= n) {
+    s_cb[tid] = rt.chunk_base[tid];
+    s_tb[tid] = rt.tok_base[tid];
+  }
+  if (tid < n) s_ly[tid] = rt.layer[tid];
   __syncthreads();
-  for (int c = tid; c < ES; c += kScanThreads) {
-    for (int b = 0; b < n_chunks; ++b) {
-      const int rho = find_entry(rt.chunk_base, rt.n, b);
-      const int T = rt.tok_base[rho + 1] - rt.tok_base[rho];
-      const int t0 = (b - rt.chunk_base[rho]) * kPermChunk;
-      const int in_chunk = min(kPermChunk, T - t0);
-      const int v = c < rt.E ? hist[(size_t)b * rt.E + c] : in_chunk;
-      running[rt.layer[rho] * ES + c] += v;
+
+  // cell (b, c): routed pairs of chunk b on expert c, or (shared slot c >= E)
+  // the chunk's tokens; *key = (layer of b's entry, c)
+  auto cell = [&](int b, int c, int* key) {
+    const int rho = find_entry(s_cb, n, b);
+    *key = s_ly[rho] * ES + c;
+    if (c < E) return (int)hist[(size_t)b * E + c];
+    return min(kPermChunk, s_tb[rho + 1] - s_tb[rho] - (b - s_cb[rho]) * kPermChunk);
+  };
+  const int win = kHistWindow / ES;  // >= 16 chunks (ES <= 1024)
+  const int n_win = (n_chunks + win - 1) / win;
+
+  // 1) per-key totals (integer LDS atomics: order-free); the last window
+  //    stays in hl
+  for (int w0 = 0; w0 < n_chunks; w0 += win) {
+    const int cells = min(win, n_chunks - w0) * ES;
+    for (int i = tid; i < cells; i += kScanThreads) {
+      int key;
+      const int v = cell(w0 + i / ES, i % ES, &key);
+      hl[i] = v;
+      atomicAdd(&running[key], v);
     }
   }
   __syncthreads();
@@ -96,7 +131,7 @@ __global__ __launch_bounds__(kScanThreads) void perm_scan_kernel(
   int local = 0;
   for (int i = k0; i < k1; ++i) local += running[i];
   int total = 0;
-  int base = block_exclusive_scan(local, scan, &total);
+  int base = block_exclusive_scan(local, wtot, &total);
   for (int i = k0; i < k1; ++i) {
     const int v = running[i];
     offsets[i] = base;
@@ -107,17 +142,18 @@ __global__ __launch_bounds__(kScanThreads) void perm_scan_kernel(
   __syncthreads();
 
   // 3) tile and group lists: ceil(M/bm) row blocks per non-empty key, keys ascending
+  auto rows_of = [&](int i) { return (i + 1 < n_keys ? running[i + 1] : total) - running[i]; };
   int local_tiles = 0, local_groups = 0;
   for (int i = k0; i < k1; ++i) {
-    const int M = offsets[i + 1] - offsets[i];
+    const int M = rows_of(i);
     local_tiles += (M + bm - 1) / bm;
     local_groups += M > 0;
   }
   int tiles_total = 0, groups_total = 0;
-  int tb = block_exclusive_scan(local_tiles, scan, &tiles_total);
-  int gb = block_exclusive_scan(local_groups, scan, &groups_total);
+  int tb = block_exclusive_scan(local_tiles, wtot, &tiles_total);
+  int gb = block_exclusive_scan(local_groups, wtot, &groups_total);
   for (int i = k0; i < k1; ++i) {
-    const int r0 = offsets[i], M = offsets[i + 1] - r0;
+    const int r0 = running[i], M = rows_of(i);
     if (M == 0) continue;
     const int4 g = make_int4(i, r0, M, tb);
     groups[gb++] = g;
@@ -130,18 +166,33 @@ __global__ __launch_bounds__(kScanThreads) void perm_scan_kernel(
     *n_tiles = min(tiles_total, max_tiles);
     *n_groups = groups_total;
   }
+  __syncthreads();  // running[] becomes the cursors below
 
-  // 4) per-chunk bases: walk chunks in order, one column per thread
-  for (int c = tid; c < ES; c += kScanThreads) {
-    for (int b = 0; b < n_chunks; ++b) {
-      const int rho = find_entry(rt.chunk_base, rt.n, b);
-      const int T = rt.tok_base[rho + 1] - rt.tok_base[rho];
-      const int t0 = (b - rt.chunk_base[rho]) * kPermChunk;
-      const int in_chunk = min(kPermChunk, T - t0);
-      const int key = rt.layer[rho] * ES + c;
-      chunk_base[(size_t)b * ES + c] = running[key];
-      running[key] += c < rt.E ? hist[(size_t)b * rt.E + c] : in_chunk;
+  // 4) per-chunk bases: for every column, the entries' chunks in order; a
+  //    key's cursor lives in LDS across entries, in a register within one
+  for (int w = 0; w < n_win; ++w) {
+    const int w0 = w * win, nw = min(win, n_chunks - w0);
+    if (n_win > 1) {
+      for (int i = tid; i < nw * ES; i += kScanThreads) {
+        int key;
+        hl[i] = cell(w0 + i / ES, i % ES, &key);
+      }
+      __syncthreads();
     }
+    for (int c = tid; c < ES; c += kScanThreads) {
+      for (int rho = 0; rho < n; ++rho) {
+        const int b_lo = max(s_cb[rho], w0), b_hi = min(s_cb[rho + 1], w0 + nw);
+        if (b_lo >= b_hi) continue;
+        const int key = s_ly[rho] * ES + c;
+        int cur = running[key];
+        for (int b = b_lo; b < b_hi; ++b) {
+          chunk_base[(size_t)b * ES + c] = cur;
+          cur += hl[(b - w0) * ES + c];
+        }
+        running[key] = cur;
+      }
+    }
+    __syncthreads();  // hl is refilled by the next window
   }
 }
 
@@ -215,9 +266,10 @@ hipError_t launch_perm_scan(const RunTable& rt, int n_chunks, const int32_t* his
                             int32_t* chunk_base, int32_t* offsets, int4* tiles,
                             int32_t* n_tiles, int4* groups, int32_t* n_groups, int bm,
                             int max_tiles, int32_t* work_ctr, hipStream_t s) {
-  const size_t smem = sizeof(int) * ((size_t)rt.L * (rt.E + rt.S) + kScanThreads);
+  if ((long)rt.L * (rt.E + rt.S) > kMaxKeys || rt.E + rt.S > kScanThreads || rt.n > EB_MAX_RUN)
+    return hipErrorInvalidValue;
   prof_start(EB_K_PERM_SCAN, s);
-  hipLaunchKernelGGL(perm_scan_kernel, dim3(1), dim3(kScanThreads), smem, s, rt, n_chunks, hist,
+  hipLaunchKernelGGL(perm_scan_kernel, dim3(1), dim3(kScanThreads), 0, s, rt, n_chunks, hist,
                      chunk_base, offsets, tiles, n_tiles, groups, n_groups, bm, max_tiles,
                      work_ctr);
   prof_stop(EB_K_PERM_SCAN, s);
