@@ -1,8 +1,10 @@
 """Load-balance sweeps over recorded routing: scheduling policies, number of
 micro-batches N, minimum combination size m and number of virtual devices
 D (the studies of Section 5: scheduling strategies, micro-batch count and
-m, EP size, and the worst-case statistic of Section 4.1), on the synthetic
-stacks.
+m, EP size, and the worst-case statistic of Section 4.1), EasyBalance on top
+of a static replicated expert placement (the orthogonality study of Section 5
+and the appendix on redundant experts), and the scheduler's cost per step
+(the context of Table 3), on the synthetic stacks.
 
 The stacks are MoE-only (x <- x + MoE_l(RMSNorm(x))), so a token's hidden
 state at layer l, and with it its experts there, depends on that token
@@ -24,6 +26,7 @@ from __future__ import annotations
 
 import argparse
 import sys
+import time
 
 import numpy as np
 
@@ -66,6 +69,81 @@ def layer_loads(routes: np.ndarray, N: int, E: int, D: int) -> np.ndarray:
         d = dev[j * T:(j + 1) * T]
         for layer in range(L):
             out[j, layer] = np.bincount(d[:, layer].ravel(), minlength=D)
+    return out
+
+
+def expert_counts(routes: np.ndarray, N: int, E: int) -> np.ndarray:
+    """Routed pairs per expert, c[j][l][e], of N contiguous micro-batches."""
+    routes = np.asarray(routes)
+    tokens, L, k = routes.shape
+    if tokens % N:
+        raise ValueError(f"{tokens} tokens into {N} micro-batches")
+    T = tokens // N
+    out = np.zeros((N, L, E), dtype=np.int64)
+    for j in range(N):
+        for layer in range(L):
+            out[j, layer] = np.bincount(routes[j * T:(j + 1) * T, layer].ravel(), minlength=E)
+    return out
+
+
+def replicated_placement(hist, D: int, replicas: int, first_device: int = 0) -> list[list[int]]:
+    """Static placement of one layer's experts on D devices from a history of
+    per-expert loads hist[E], in the manner of EPLB-style replication (the
+    placement of the orthogonality study; the heuristic is this module's own):
+
+      * the `replicas` hottest experts (history load descending, ties ->
+        lower id) get one extra copy each, and a copy carries hist[e] /
+        copies(e) of expected load;
+      * copies are placed largest expected load first (ties -> lower expert
+        id) on the device with the least expected load so far that has a free
+        slot, preferring devices that hold no copy of the same expert (ties
+        -> the first device in the order first_device, first_device + 1, ...
+        mod D); every device has (E + replicas) / D slots.
+
+    Returns slots[d], the logical experts device d holds (ascending)."""
+    hist = np.asarray(hist, dtype=np.int64)
+    E = hist.shape[0]
+    if D < 1 or not 0 <= replicas <= E or (E + replicas) % D:
+        raise ValueError(f"E={E} + replicas={replicas} not a multiple of D={D}")
+    per = (E + replicas) // D
+    order = sorted(range(E), key=lambda e: (-hist[e], e))
+    copies = np.ones(E, dtype=np.int64)
+    copies[order[:replicas]] = 2
+    items = [(e, c) for e in range(E) for c in range(int(copies[e]))]
+    # expected load hist/copies, compared exactly as hist[a]*copies[b] vs hist[b]*copies[a]
+    items.sort(key=lambda ec: (-(hist[ec[0]] * 2 // copies[ec[0]]), ec[0], ec[1]))
+    load2 = np.zeros(D, dtype=np.int64)   # twice the expected load (integer)
+    slots = [[] for _ in range(D)]
+    for e, _ in items:
+        free = [d for d in range(D) if len(slots[d]) < per]
+        fresh = [d for d in free if e not in slots[d]]
+        d = min(fresh or free, key=lambda x: (load2[x], (x - first_device) % D))
+        slots[d].append(e)
+        load2[d] += hist[e] * 2 // copies[e]
+    return [sorted(s) for s in slots]
+
+
+def placed_loads(counts: np.ndarray, placements) -> np.ndarray:
+    """Per-device load w[j][l][d] under per-layer placements (placements[l] =
+    slots as from replicated_placement): expert e's pairs are split evenly
+    over its copies, the first c mod r copies in device order taking one
+    more."""
+    counts = np.asarray(counts, dtype=np.int64)
+    N, L, E = counts.shape
+    D = len(placements[0])
+    out = np.zeros((N, L, D), dtype=np.int64)
+    for layer in range(L):
+        holders = [[] for _ in range(E)]
+        for d, held in enumerate(placements[layer]):
+            for e in held:
+                holders[e].append(d)
+        if any(not h for h in holders):
+            raise ValueError(f"layer {layer}: an expert has no device")
+        for e in range(E):
+            r = len(holders[e])
+            c = counts[:, layer, e]
+            for i, d in enumerate(holders[e]):
+                out[:, layer, d] += c // r + (c % r > i)
     return out
 
 
@@ -166,6 +244,41 @@ def report(routes: np.ndarray, cfg) -> str:
     parts.append(f"\nVirtual devices D (N = {cfg.N}, m = {m_def(cfg.N)}):\n")
     parts.append(_table(rows, ["D", "policy", "under-utilization"],
                         lambda r: [str(r["D"]), r["policy"], f"{r['under_util']:.3f}"]))
+    # EasyBalance on a static replicated placement; history = the batch's own
+    # per-layer expert counts (the most favourable history a placement can have)
+    counts = expert_counts(routes, cfg.N, cfg.E)
+    hist = counts.sum(axis=0)
+    # Ties at device 0 in every layer put every layer's hottest expert on one
+    # device (its peaks coincide: the worst case of Section 4.1); rotating the
+    # tie order by layer does not.
+    mappings = [("contiguous, E/D experts per device", cfg.E, layer_loads(routes, cfg.N, cfg.E, cfg.D))]
+    for reps in (0, cfg.D):
+        for rot in (False, True):
+            pl = [replicated_placement(hist[layer], cfg.D, reps, layer % cfg.D if rot else 0)
+                  for layer in range(cfg.L)]
+            ties = "ties rotated by layer" if rot else "ties at device 0"
+            mappings.append((f"placed from history, {cfg.E + reps} physical experts, {ties}",
+                             cfg.E + reps, placed_loads(counts, pl)))
+    rows = []
+    for name, _, w in mappings:
+        r = {"mapping": name}
+        for pol in ("lockstep", "maxutil", "cumutil", "diffpeak"):
+            r[pol] = metrics.summary(run_policy(w, pol, m_def(cfg.N)))["idle_fraction"]
+        rows.append(r)
+    parts.append(f"\nStatic placement + EasyBalance (N = {cfg.N}, D = {cfg.D}, m = {m_def(cfg.N)}; "
+                 "under-utilization):\n")
+    parts.append(_table(rows, ["mapping", "lock-step", "MaxUtil", "CumUtil", "DiffPeak"],
+                        lambda r: [r["mapping"]] + [f"{r[p]:.3f}" for p in
+                                                    ("lockstep", "maxutil", "cumutil", "diffpeak")]))
+    # scheduler cost per decision at the stack's own N, D, m
+    w = mappings[0][2]
+    cost = []
+    for pol in ("maxutil", "cumutil", "diffpeak"):
+        t0 = time.perf_counter()
+        n_steps = len(run_policy(w, pol, m_def(cfg.N)))
+        cost.append(f"{pol} {(time.perf_counter() - t0) / n_steps * 1e6:.0f} µs")
+    parts.append("\nHost time per scheduling decision (one replayed pass, including the Python "
+                 "replay loop and the binding call): " + ", ".join(cost) + "\n")
     # worst-case windows over the whole batch's per-layer loads
     whole = layer_loads(routes, 1, cfg.E, cfg.D)[0]
     stats = []

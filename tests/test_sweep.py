@@ -87,3 +87,49 @@ def test_sweep_rows_shape():
     assert len(rows) == sum(3 * n + 2 for n in (2, 4)) * 2
     for row in rows:
         assert 0.0 <= row["under_util"] < 1.0 and row["max_over_mean"] >= 1.0
+
+
+def test_replicated_placement_hand_worked():
+    # history [10, 1, 1, 8] on two devices: largest first onto the least-loaded
+    # device with a free slot (two slots each)
+    assert sweep.replicated_placement([10, 1, 1, 8], 2, 0) == [[0, 2], [1, 3]]
+    assert sweep.replicated_placement([10, 1, 1, 8], 2, 0, first_device=1) == [[1, 3], [0, 2]]
+    # two replicas: experts 0 and 3 get a second copy on the other device
+    # (expected loads 5, 5, 4, 4, 1, 1; three slots each)
+    assert sweep.replicated_placement([10, 1, 1, 8], 2, 2) == [[0, 1, 3], [0, 2, 3]]
+    with pytest.raises(ValueError):
+        sweep.replicated_placement([1, 2, 3], 2, 0)
+
+
+def test_replicated_placement_invariants():
+    rng = np.random.default_rng(7)
+    for E, D, reps in ((8, 8, 0), (8, 8, 8), (60, 4, 4), (64, 8, 8), (16, 4, 0)):
+        hist = rng.integers(0, 1000, size=E)
+        hist[rng.integers(0, E)] = hist[rng.integers(0, E)]  # a tie
+        for first in (0, D - 1):
+            slots = sweep.replicated_placement(hist, D, reps, first)
+            assert [len(s) for s in slots] == [(E + reps) // D] * D
+            held = np.bincount(np.concatenate(slots), minlength=E)
+            order = sorted(range(E), key=lambda e: (-hist[e], e))
+            assert sorted(np.flatnonzero(held == 2)) == sorted(order[:reps])
+            assert set(np.unique(held)) <= {1, 2}
+            for s in slots:  # the copies of one expert sit on different devices
+                assert len(set(s)) == len(s)
+
+
+def test_placed_loads_split_and_contiguous_case():
+    rng = np.random.default_rng(9)
+    r = _routes(rng, 32, 3, 2, 8)
+    counts = sweep.expert_counts(r, 4, 8)
+    assert counts.shape == (4, 3, 8) and counts.sum() == 32 * 3 * 2
+    # the contiguous mapping reproduces layer_loads
+    contiguous = [[list(range(d * 2, d * 2 + 2)) for d in range(4)]] * 3
+    assert np.array_equal(sweep.placed_loads(counts, contiguous), sweep.layer_loads(r, 4, 8, 4))
+    # a replicated expert's pairs split evenly, the lower device taking the extra one
+    c = np.zeros((1, 1, 3), np.int64)
+    c[0, 0] = [5, 2, 4]
+    got = sweep.placed_loads(c, [[[0, 1], [0, 2]]])
+    assert got.tolist() == [[[3 + 2, 2 + 4]]]
+    placements = [sweep.replicated_placement(counts.sum(axis=0)[l], 4, 4, l) for l in range(3)]
+    w = sweep.placed_loads(counts, placements)
+    assert np.array_equal(w.sum(axis=2), counts.sum(axis=2))  # pairs are conserved
