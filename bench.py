@@ -128,7 +128,7 @@ def main() -> int:
 
     from paper_2608_07964_amd import binding as B
     from paper_2608_07964_amd import metrics
-    from paper_2608_07964_amd.driver import Stack
+    from paper_2608_07964_amd.driver import Stack, pack_expert_weights
     from synth import BY_NAME
     from synth.device import DeviceInputs
 
@@ -141,6 +141,11 @@ def main() -> int:
     torch.cuda.synchronize()
     log(f"{cfg.name}: inputs generated in HBM in {time.perf_counter() - t0:.2f}s "
         f"({inp.weight_bytes() / 1e9:.1f} GB of expert weights)")
+    t0 = time.perf_counter()
+    pack_expert_weights(B.make_desc(cfg.L, cfg.H, cfg.F, cfg.E, cfg.k, cfg.S, cfg.D, cfg.dtype, cfg.eps,
+                                    cfg.norm_topk), inp.W_gu, inp.W_dn)
+    torch.cuda.synchronize()
+    log(f"{cfg.name}: expert weights packed for the grouped GEMMs in {time.perf_counter() - t0:.2f}s")
     st = Stack(L=cfg.L, H=cfg.H, F=cfg.F, E=cfg.E, k=cfg.k, S=cfg.S, D=cfg.D, N=cfg.N, T=cfg.T,
                dtype=cfg.dtype, x=inp.x0.clone(), gain=inp.g, Wg=inp.Wg, bias=inp.bias,
                W_gu=inp.W_gu, W_dn=inp.W_dn, eps=cfg.eps, norm_topk=cfg.norm_topk, device=dev)

@@ -23,12 +23,14 @@
  *  - Streams: `stream` is a hipStream_t passed as void* (NULL = null stream).
  *    Device calls only enqueue work on it and never synchronize; the caller
  *    orders calls on one stream or with events.
- *  - Layouts are row-major and densely packed.  "dtype" is the model's storage
- *    type (EB_DTYPE_F32 or EB_DTYPE_BF16, bf16 as raw 16-bit patterns);
- *    accumulation is always fp32.
+ *  - Layouts are row-major and densely packed, except the expert weights
+ *    that easybalance_moe_step reads (see easybalance_pack_weights).
+ *    "dtype" is the model's storage type (EB_DTYPE_F32 or EB_DTYPE_BF16,
+ *    bf16 as raw 16-bit patterns); accumulation is always fp32.
  *  - Shape limits (EB_ERR_UNSUPPORTED otherwise): H % 256 == 0,
  *    F % 128 == 0, 1 <= k <= E, E + S <= 1024, k + S <= 16, E % D == 0,
- *    L <= EB_MAX_LAYERS, L * (E + S) <= 15360; bf16 stacks: E <= 256.
+ *    L <= EB_MAX_LAYERS, L * (E + S) <= 15360; bf16 stacks: E <= 256 and
+ *    2F * H * 2 bytes < 2 GiB (one gate/up matrix).
  */
 #ifndef EASYBALANCE_H
 #define EASYBALANCE_H
@@ -52,6 +54,9 @@ extern "C" {
 #define EB_POLICY_MAXUTIL 0
 #define EB_POLICY_CUMUTIL 1
 #define EB_POLICY_DIFFPEAK 2
+#define EB_WEIGHTS_GATE_UP 0     /* easybalance_pack_weights kinds */
+#define EB_WEIGHTS_DOWN 1
+
 #define EB_POLICY_LOCKSTEP 3    /* easybalance_run_pass only: every pooled
                                    micro-batch every step (per-layer baseline) */
 
@@ -198,8 +203,10 @@ int easybalance_moe_step_workspace_size(const eb_model_desc* desc, int32_t n_run
  * in, so results do not depend on the schedule (batch invariance).
  *
  * run      host [n_run] (1 <= n_run <= EB_MAX_RUN); `run` order defines q
- * W_gu     host [L] of device pointers, each [E+S][2F][H] dtype
- * W_dn     host [L] of device pointers, each [E+S][H][F] dtype
+ * W_gu     host [L] of device pointers, each the E+S matrices [2F][H] dtype
+ *          as easybalance_pack_weights(EB_WEIGHTS_GATE_UP) wrote them
+ * W_dn     host [L] of device pointers, each the E+S matrices [H][F] dtype
+ *          as easybalance_pack_weights(EB_WEIGHTS_DOWN) wrote them
  * ws       device workspace of ws_bytes >= easybalance_moe_step_workspace_size
  *          (else EB_ERR_WORKSPACE_TOO_SMALL); 256-byte aligned
  * o_out    device [P][H] dtype: expert outputs at grouped positions
@@ -211,6 +218,29 @@ int easybalance_moe_step(const eb_model_desc* desc, int32_t n_run, const eb_work
                          const void* const* W_gu, const void* const* W_dn, void* ws,
                          size_t ws_bytes, void* o_out, int32_t* inv_out,
                          const eb_step_views* views, void* stream);
+
+/*
+ * easybalance_pack_weights -- expert weights into the layout the grouped
+ * GEMMs of easybalance_moe_step stream (once, when the weights are loaded;
+ * the expert computation of Section 2.1 / Eq. 1 is unchanged, only where its
+ * weights sit in memory).
+ *
+ * kind  EB_WEIGHTS_GATE_UP: n matrices [2F][H] (rows 0..F-1 the gate
+ *       projection, F..2F-1 the up projection), row-major, back to back;
+ *       EB_WEIGHTS_DOWN: n matrices [H][F], row-major, back to back.
+ * src   device, the row-major matrices (dtype of desc); unchanged
+ * dst   device, same size, written; must not overlap src; 16-byte aligned
+ * bf16: each N x K matrix (N its rows) becomes (K/64) x (N/256) blocks of
+ *   256 x 64 elements, block (s, t) at index s*(N/256) + t with K columns
+ *   64s .. 64s+63 of column tile t; block row r is weight row 256t + r
+ *   (down) or 128t + 32(r/64) + (r%64 < 32 ? r%64 : r%64 - 32 + F) (gate/up);
+ *   its 16-byte chunk at position c holds K columns 64s + 8(c ^ ((r>>1)&7))
+ *   .. +7.  fp32: dst is a copy of src (row-major).
+ * Enqueued on `stream`; errors: EB_ERR_INVALID_ARG (bad kind, n < 0, NULL,
+ * overlap, misalignment), EB_ERR_HIP.
+ */
+int easybalance_pack_weights(const eb_model_desc* desc, int32_t kind, int32_t n, const void* src,
+                             void* dst, void* stream);
 
 /*
  * easybalance_combine -- the weighted sum of Eq. (1) plus the residual of

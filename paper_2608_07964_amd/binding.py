@@ -23,6 +23,7 @@ EB_ERR_HIP = -3
 EB_ERR_WORKSPACE_TOO_SMALL = -4
 EB_DTYPE_F32, EB_DTYPE_BF16 = 0, 1
 EB_POLICY_MAXUTIL, EB_POLICY_CUMUTIL, EB_POLICY_DIFFPEAK, EB_POLICY_LOCKSTEP = 0, 1, 2, 3
+EB_WEIGHTS_GATE_UP, EB_WEIGHTS_DOWN = 0, 1
 EB_MAX_POOL = 64
 EB_MAXUTIL_MAX_POOL = 20
 KERNEL_NAMES = ["route_norm", "route_logits", "route_topk", "perm_count", "perm_scan",
@@ -33,7 +34,7 @@ EB_PROFILE_ALL = (1 << EB_NUM_KERNELS) - 1
 EXPORTS = ["easybalance_version", "easybalance_last_error", "easybalance_route",
            "easybalance_schedule", "easybalance_moe_step_workspace_size", "easybalance_moe_step",
            "easybalance_combine", "easybalance_profile_begin", "easybalance_profile_end",
-           "easybalance_pass_state_size", "easybalance_run_pass"]
+           "easybalance_pass_state_size", "easybalance_run_pass", "easybalance_pack_weights"]
 
 
 class eb_model_desc(ctypes.Structure):
@@ -96,6 +97,8 @@ def lib() -> ctypes.CDLL:
                                        I32, ctypes.POINTER(ctypes.c_int32), U64P,
                                        ctypes.POINTER(ctypes.c_int32), I64P,
                                        ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32), P]
+    l.easybalance_pack_weights.restype = ctypes.c_int
+    l.easybalance_pack_weights.argtypes = [D, I32, I32, P, P, P]
     l.easybalance_profile_begin.restype = ctypes.c_int
     l.easybalance_profile_begin.argtypes = [ctypes.c_uint32]
     l.easybalance_profile_end.restype = ctypes.c_int
@@ -189,6 +192,11 @@ def easybalance_moe_step(desc, run, n_run, W_gu, W_dn, ws, ws_bytes, o_out, inv_
     _check("easybalance_moe_step", lib().easybalance_moe_step(
         ctypes.byref(desc), n_run, run, gu, dn, _ptr(ws), ws_bytes, _ptr(o_out), _ptr(inv_out),
         v, stream))
+
+
+def easybalance_pack_weights(desc, kind, n, src, dst, stream=None) -> None:
+    _check("easybalance_pack_weights", lib().easybalance_pack_weights(
+        ctypes.byref(desc), kind, n, _ptr(src), _ptr(dst), stream))
 
 
 def easybalance_combine(desc, run, n_run, x_list, o, inv, stream=None) -> None:

@@ -38,6 +38,8 @@ int check_desc(const eb_model_desc* d) {
     return set_error(EB_ERR_UNSUPPORTED, "bf16 router supports E <= 256 (E=%d)", d->E);
   if (d->k + d->S > kMaxSlots) return set_error(EB_ERR_UNSUPPORTED, "k+S=%d > %d", d->k + d->S, kMaxSlots);
   if (d->L > EB_MAX_LAYERS) return set_error(EB_ERR_UNSUPPORTED, "L=%d > %d", d->L, EB_MAX_LAYERS);
+  if (d->dtype == EB_DTYPE_BF16 && 2LL * d->F * d->H * 2 >= (1LL << 31))
+    return set_error(EB_ERR_UNSUPPORTED, "an expert's gate/up matrix (2F x H bf16) must be < 2 GiB");
   if ((long)d->L * (d->E + d->S) > 15360)
     return set_error(EB_ERR_UNSUPPORTED, "L*(E+S)=%ld > 15360", (long)d->L * (d->E + d->S));
   return EB_OK;
@@ -344,6 +346,26 @@ int easybalance_combine(const eb_model_desc* desc, int32_t n_run, const eb_work*
   return hip_status(launch_combine(rt, (int)tokens, desc->dtype, o, inv,
                                    static_cast<hipStream_t>(stream)),
                     "combine");
+}
+
+int easybalance_pack_weights(const eb_model_desc* desc, int32_t kind, int32_t n, const void* src,
+                            void* dst, void* stream) {
+  int rc = check_desc(desc);
+  if (rc) return rc;
+  if (kind != EB_WEIGHTS_GATE_UP && kind != EB_WEIGHTS_DOWN)
+    return set_error(EB_ERR_INVALID_ARG, "kind %d is not EB_WEIGHTS_GATE_UP/DOWN", kind);
+  if (n < 0) return set_error(EB_ERR_INVALID_ARG, "n=%d < 0", n);
+  if (n == 0) return EB_OK;
+  if (src == nullptr || dst == nullptr) return set_error(EB_ERR_INVALID_ARG, "src/dst is NULL");
+  const int N = kind == EB_WEIGHTS_GATE_UP ? 2 * desc->F : desc->H;
+  const int K = kind == EB_WEIGHTS_GATE_UP ? desc->H : desc->F;
+  const size_t bytes = (size_t)n * N * K * (desc->dtype == EB_DTYPE_BF16 ? 2 : 4);
+  const uintptr_t s0 = reinterpret_cast<uintptr_t>(src), d0 = reinterpret_cast<uintptr_t>(dst);
+  if (s0 < d0 + bytes && d0 < s0 + bytes) return set_error(EB_ERR_INVALID_ARG, "src and dst overlap");
+  if ((s0 | d0) % 16 != 0) return set_error(EB_ERR_INVALID_ARG, "src/dst not 16-byte aligned");
+  return hip_status(launch_pack_weights(desc->dtype, kind == EB_WEIGHTS_GATE_UP, n, N, K, desc->F, src,
+                                        dst, static_cast<hipStream_t>(stream)),
+                    "pack_weights");
 }
 
 int easybalance_profile_begin(uint32_t kernel_mask) {

@@ -103,6 +103,11 @@ hipError_t launch_perm_scatter(const RunTable& rt, int n_chunks, int P, int elem
 // Row-block height of the grouped GEMM tiles for a dtype.
 int gemm_bm(int dtype);
 
+// Expert weights in the layout the grouped GEMMs read (bf16: packed blocks,
+// see gemm.hip; fp32: row-major, a copy).  n matrices of N x K.
+hipError_t launch_pack_weights(int dtype, int gateup, int n, int N, int K, int F, const void* src,
+                               void* dst, hipStream_t s);
+
 hipError_t launch_gateup(int dtype, const GroupedProblem& p, const WeightTable& wt,
                          const void* a_perm, void* h, hipStream_t s);
 hipError_t launch_down(int dtype, const GroupedProblem& p, const WeightTable& wt,

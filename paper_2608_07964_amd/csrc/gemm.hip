@@ -13,7 +13,11 @@
 // of the MFMAs; persistent, XCD-aware work distribution.  The gate/up B tile
 // interleaves the gate rows and the matching up rows per wavefront column,
 // so each lane holds gate and up of the same (row, f) and SwiGLU runs in
-// registers.
+// registers.  The expert weights are read in the packed layout that
+// pack_bf16_kernel writes once (see there): every B stage of a tile is one
+// contiguous 32 KB block holding exactly the bytes its LDS slot receives,
+// and the blocks of one K stage of all of an expert's column tiles are
+// adjacent, so concurrent items stream neighbouring blocks.
 //
 // Every output accumulates its K dimension in 16-wide MFMA steps in ascending
 // order, whatever tile or group its row sits in: rows give the same bits
@@ -112,20 +116,23 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, 
 }
 
 // Load slots: in every stage wave w fills A rows (BM/4) w + 8 j + l/8
-// (j < BM/32) and B rows 64 w + 8 j + l/8 (j < 8) of the tile, lane l at
-// physical chunk l % 8, i.e. logical chunk (l % 8) ^ ((r >> 1) & 7), which is
-// c0 for even j and c0 ^ 4 for odd j (every block base is a multiple of 16
-// rows).  A load's byte offset is a per-lane part (row l/8 of the block and
-// the chunk, by parity of j) plus a wave-uniform part (the block's first
-// global row and the stage's K offset) passed as soffset.  A rows past the
-// buffer's end read zeros; rows past the group's end are loaded but their
-// results are discarded.
+// (j < BM/32) of the tile, lane l at physical chunk l % 8, i.e. logical chunk
+// (l % 8) ^ ((r >> 1) & 7), which is c0 for even j and c0 ^ 4 for odd j
+// (every block base is a multiple of 16 rows).  An A load's byte offset is a
+// per-lane part (row l/8 of the block and the chunk, by parity of j) plus a
+// wave-uniform part (the block's first row and the stage's K offset) passed
+// as soffset.  A rows past the buffer's end read zeros; rows past the group's
+// end are loaded but their results are discarded.  B comes packed: wave w's
+// load j of stage s copies the 1 KB at byte 4096 w + 1024 j of the stage's
+// 32 KB block (LDS rows 32 w + 8 j .. + 7), lane l its 16 bytes at 16 l.
 struct KLoop {
   bf16_t* smem;
-  __amdgpu_buffer_rsrc_t ra, rb;   // buffer descriptors of the A tile and the expert's B
-  int a_lane[2], b_lane[2];        // per-lane byte offsets for even / odd j
+  __amdgpu_buffer_rsrc_t ra, rb;   // buffer descriptors of the A tile and the expert's packed B
+  int a_lane[2];                   // per-lane A byte offsets for even / odd j
+  int b_lane;                      // per-lane B byte offset (16 l)
   int a_row0;                      // first A row (within the tile) of the wave's load blocks
-  int b_row[kBLoads];              // first global B row of each of the wave's load blocks
+  int b_tile;                      // byte offset of the wave's first B KB at the item's first stage
+  int b_stage;                     // bytes from one K stage's blocks to the next one's
   int row_bytes;                   // K * 2
   int lds_a_load, lds_b_load;      // LDS element offsets of the wave's first A / B load rows
   int lds_a, lds_b;                // LDS element offsets of this lane's fragment rows (chunk-free)
@@ -151,8 +158,8 @@ __device__ __forceinline__ void load_a(const KLoop& L, int s, int slot, int j) {
 }
 template <class C>
 __device__ __forceinline__ void load_b(const KLoop& L, int s, int slot, int j) {
-  load16_lds(L.rb, L.smem + C::B_RING + slot * C::B_ELEMS + L.lds_b_load + j * 8 * BK, L.b_lane[j & 1],
-             L.b_row[j] * L.row_bytes + s * BK * 2);
+  load16_lds(L.rb, L.smem + C::B_RING + slot * C::B_ELEMS + L.lds_b_load + j * 8 * BK, L.b_lane,
+             L.b_tile + s * L.b_stage + j * 1024);
 }
 template <class C>
 __device__ __forceinline__ void issue_a(const KLoop& L, int s, int slot) {
@@ -448,31 +455,18 @@ __device__ __forceinline__ void run_item(const GroupedProblem& p, bf16_t* smem, 
   KLoop kl;
   kl.smem = smem;
   kl.ra = buffer_rsrc(Atile, (uint32_t)(a_rows * K * 2 - k_off * 2));
-  kl.rb = buffer_rsrc(Bbase + k_off, (uint32_t)((MODE == MODE_GATEUP ? 2 * p.F : p.H) * K * 2 - k_off * 2));
+  const int n_rows = MODE == MODE_GATEUP ? 2 * p.F : p.H;  // the expert matrix is n_rows x K
+  kl.rb = buffer_rsrc(Bbase, (uint32_t)n_rows * (uint32_t)K * 2u);
   kl.row_bytes = K * 2;
   {
-    // swizzle of the wave's first load row of each operand; odd j flips bit 2
+    // swizzle of the wave's first A load row; odd j flips bit 2
     const int ca = lp ^ ((((C::BM / kWaves) * wave + lr) >> 1) & 7);
-    const int cb = lp ^ ((((BN / kWaves) * wave + lr) >> 1) & 7);
     kl.a_lane[0] = lr * K * 2 + ca * 16;
     kl.a_lane[1] = lr * K * 2 + (ca ^ 4) * 16;
-    kl.b_lane[0] = lr * K * 2 + cb * 16;
-    kl.b_lane[1] = lr * K * 2 + (cb ^ 4) * 16;
     kl.a_row0 = (C::BM / kWaves) * wave;
-#pragma unroll
-    for (int j = 0; j < kBLoads; ++j) {
-      if (MODE == MODE_GATEUP) {
-        // wavefront column wc owns TN/2 gate rows f and the TN/2 matching up
-        // rows F+f, f = ni*128 + wc*TN/2 + q; LDS B row 64 w + 8 j sits in
-        // column (64 w) / TN at position q0 = (64 w) % TN + 8 j
-        const int r = (BN / kWaves) * wave + 8 * j;
-        const int wc = r / C::TN, q = r % C::TN;
-        const int half = C::TN / 2;
-        kl.b_row[j] = ni * (BN / 2) + wc * half + (q < half ? q : q - half + p.F);
-      } else {
-        kl.b_row[j] = ni * BN + (BN / kWaves) * wave + 8 * j;
-      }
-    }
+    kl.b_lane = lane * 16;
+    kl.b_stage = (n_rows / BN) * (BN * BK * 2);
+    kl.b_tile = ks0 * kl.b_stage + ni * (BN * BK * 2) + wave * (BN / kWaves) * BK * 2;
   }
   kl.lds_a_load = (C::BM / kWaves) * wave * BK;
   kl.lds_b_load = (BN / kWaves) * wave * BK;
@@ -691,9 +685,58 @@ __global__ __launch_bounds__(256) void split_sum_kernel(const float* __restrict_
   *reinterpret_cast<uint2*>(o + i) = u;
 }
 
+// Packed bf16 expert weights.  An expert matrix W [N][K] (gate/up: N = 2F
+// rows, gate rows f then up rows F + f, K = H; down: N = H, K = F) becomes
+// (K / 64) x (N / 256) blocks of 256 x 64 elements (32 KB), block (s, t) at
+// index s * (N / 256) + t holding K columns 64 s .. 64 s + 63 of column tile
+// t.  Block row r is weight row
+//   down:     256 t + r
+//   gate/up:  128 t + 32 (r / 64) + (r % 64 < 32 ? r % 64 : r % 64 - 32 + F)
+// (the 64 rows of wavefront column r / 64 are 32 gate rows and the matching
+// 32 up rows), and its 16-byte chunk at position c holds the 8 K columns
+// 64 s + 8 (c ^ ((r >> 1) & 7)) .. + 7 (the LDS swizzle of the ring).
+// One thread per 16-byte chunk of dst; n matrices back to back.
+__global__ __launch_bounds__(256) void pack_bf16_kernel(const uint4* __restrict__ src,
+                                                        uint4* __restrict__ dst, long long chunks,
+                                                        int N, int K, int F, int gateup) {
+  const long long per_mat = (long long)N * K / 8;
+  const int ntiles = N / BN;
+  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < chunks;
+       i += (long long)gridDim.x * blockDim.x) {
+    const long long mat = i / per_mat;
+    const int rem = (int)(i - mat * per_mat);
+    const int blk = rem / (BN * BK / 8), in = rem - blk * (BN * BK / 8);
+    const int r = in >> 3, c = in & 7;
+    const int st = blk / ntiles, t = blk - st * ntiles;
+    int row;
+    if (gateup) {
+      const int q = r & 63;
+      row = t * (BN / 2) + (r >> 6) * 32 + (q < 32 ? q : q - 32 + F);
+    } else {
+      row = t * BN + r;
+    }
+    const int col = st * BK + 8 * swz(r, c);
+    dst[i] = src[mat * per_mat + ((long long)row * K + col) / 8];
+  }
+}
+
 }  // namespace
 
 int gemm_bm(int dtype) { return dtype == EB_DTYPE_BF16 ? BM : FBM; }
+
+hipError_t launch_pack_weights(int dtype, int gateup, int n, int N, int K, int F, const void* src,
+                               void* dst, hipStream_t s) {
+  const size_t elem = dtype == EB_DTYPE_BF16 ? 2 : 4;
+  const size_t bytes = (size_t)n * N * K * elem;
+  if (bytes == 0) return hipSuccess;
+  if (dtype != EB_DTYPE_BF16) return hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, s);
+  const long long chunks = (long long)(bytes / 16);
+  const long long want = (chunks + 255) / 256;
+  const unsigned grid = (unsigned)(want < 65536 ? want : 65536);
+  hipLaunchKernelGGL(pack_bf16_kernel, dim3(grid), dim3(256), 0, s, static_cast<const uint4*>(src),
+                     static_cast<uint4*>(dst), chunks, N, K, F, gateup);
+  return hipGetLastError();
+}
 
 static int persistent_grid() {
   static int grid = 0;

@@ -17,6 +17,7 @@ library's kernels (or its host scheduler).
 from __future__ import annotations
 
 import dataclasses
+import weakref
 
 import numpy as np
 import torch
@@ -25,6 +26,32 @@ from . import binding as B
 
 POLICIES = {"maxutil": B.EB_POLICY_MAXUTIL, "cumutil": B.EB_POLICY_CUMUTIL,
             "diffpeak": B.EB_POLICY_DIFFPEAK, "lockstep": None}
+
+
+# tensors whose contents are packed expert weights (id -> tensor)
+_packed: "weakref.WeakValueDictionary[int, torch.Tensor]" = weakref.WeakValueDictionary()
+
+
+def is_packed(t: torch.Tensor) -> bool:
+    return _packed.get(id(t)) is t
+
+
+def pack_expert_weights(desc, W_gu, W_dn) -> None:
+    """Relays every layer's expert weights, in place, into the layout the
+    grouped GEMMs read (easybalance_pack_weights), through a one-layer
+    temporary copy.  W_gu [L] -> [E+S][2F][H], W_dn [L] -> [E+S][H][F],
+    row-major on entry.  Each tensor is packed once."""
+    for layers, kind in ((W_gu, B.EB_WEIGHTS_GATE_UP), (W_dn, B.EB_WEIGHTS_DOWN)):
+        for t in layers:
+            if is_packed(t):
+                raise ValueError("these expert weights are already packed")
+            if not (t.is_cuda and t.is_contiguous()):
+                raise ValueError("expert weights must be contiguous device tensors")
+            stream = torch.cuda.current_stream(t.device)
+            src = t.clone()
+            B.easybalance_pack_weights(desc, kind, t.shape[0], src, t, stream.cuda_stream)
+            del src  # freed in stream order, after the pack
+            _packed[id(t)] = t
 
 
 @dataclasses.dataclass
@@ -40,7 +67,8 @@ class Stack:
 
     x [N][T][H] fp32 is updated in place.  Inputs: gain [L][H] fp32,
     Wg [L] -> [E][H], bias [L][E] fp32, W_gu [L] -> [E+S][2F][H],
-    W_dn [L] -> [E+S][H][F] (dtype of the stack).
+    W_dn [L] -> [E+S][H][F] (dtype of the stack), the expert weights packed
+    by pack_expert_weights.
     """
 
     def __init__(self, *, L, H, F, E, k, S, D, N, T, dtype, x, gain, Wg, bias, W_gu, W_dn,
@@ -53,6 +81,8 @@ class Stack:
         tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
         self.x, self.gain, self.Wg, self.bias, self.W_gu, self.W_dn = x, gain, Wg, bias, W_gu, W_dn
         assert x.shape == (N, T, H) and x.dtype == torch.float32 and x.is_contiguous()
+        if not all(is_packed(t) for t in list(W_gu) + list(W_dn)):
+            raise ValueError("expert weights must be packed with pack_expert_weights first")
         self.a = torch.empty(N, T, H, dtype=tdt, device=self.dev)
         self.logits = torch.empty(N, T, E, dtype=torch.float32, device=self.dev)
         self.idx = torch.empty(N, T, k, dtype=torch.int32, device=self.dev)

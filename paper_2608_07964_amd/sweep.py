@@ -304,10 +304,12 @@ def main(argv=None) -> int:
     else:
         import torch
         from synth.device import DeviceInputs
-        from .driver import Stack
+        from .driver import Stack, pack_expert_weights
         B.lib()
         dev = "cuda:0"
         inp = DeviceInputs(cfg, dev)
+        pack_expert_weights(B.make_desc(cfg.L, cfg.H, cfg.F, cfg.E, cfg.k, cfg.S, cfg.D, cfg.dtype,
+                                        cfg.eps, cfg.norm_topk), inp.W_gu, inp.W_dn)
         st = Stack(L=cfg.L, H=cfg.H, F=cfg.F, E=cfg.E, k=cfg.k, S=cfg.S, D=cfg.D, N=cfg.N, T=cfg.T,
                    dtype=cfg.dtype, x=inp.x0.clone(), gain=inp.g, Wg=inp.Wg, bias=inp.bias,
                    W_gu=inp.W_gu, W_dn=inp.W_dn, eps=cfg.eps, norm_topk=cfg.norm_topk, device=dev)

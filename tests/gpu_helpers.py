@@ -50,9 +50,21 @@ def log(msg: str) -> None:
     sys.stdout.flush()
 
 
+def ensure_packed(cfg, inp: DeviceInputs) -> DeviceInputs:
+    """Packs the inputs' expert weights, once, into the layout the library's
+    grouped GEMMs read (the host oracle regenerates its own row-major copies)."""
+    from paper_2608_07964_amd import binding as B
+    from paper_2608_07964_amd.driver import is_packed, pack_expert_weights
+    if inp.W_gu and not is_packed(inp.W_gu[0]):
+        desc = B.make_desc(cfg.L, cfg.H, cfg.F, cfg.E, cfg.k, cfg.S, cfg.D, cfg.dtype, cfg.eps,
+                           cfg.norm_topk)
+        pack_expert_weights(desc, inp.W_gu, inp.W_dn)
+    return inp
+
+
 def make_stack(cfg, device="cuda:0", inputs: DeviceInputs | None = None):
     from paper_2608_07964_amd.driver import Stack
-    inp = inputs or DeviceInputs(cfg, device)
+    inp = ensure_packed(cfg, inputs or DeviceInputs(cfg, device))
     x = inp.x0.clone()
     st = Stack(L=cfg.L, H=cfg.H, F=cfg.F, E=cfg.E, k=cfg.k, S=cfg.S, D=cfg.D, N=cfg.N, T=cfg.T,
                dtype=cfg.dtype, x=x, gain=inp.g, Wg=inp.Wg, bias=inp.bias, W_gu=inp.W_gu,

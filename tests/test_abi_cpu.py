@@ -150,3 +150,21 @@ def test_run_pass_rejects_bad_arguments_before_touching_the_gpu():
     with pytest.raises(B.EasyBalanceError) as e:   # m < 1
         B.easybalance_run_pass(*args, B.EB_POLICY_MAXUTIL, 0, fake, need)
     assert e.value.code == B.EB_ERR_INVALID_ARG
+
+
+def test_pack_weights_rejects_bad_arguments_before_touching_the_gpu():
+    d = B.make_desc(2, 256, 128, 8, 2, 0, 4, "bf16")
+    fake, gu_bytes = 1 << 20, 256 * 256 * 2  # one [2F][H] bf16 matrix
+    B.easybalance_pack_weights(d, B.EB_WEIGHTS_GATE_UP, 0, None, None)  # nothing to do
+    for args, code in [((7, 1, fake, fake + gu_bytes), B.EB_ERR_INVALID_ARG),        # kind
+                       ((B.EB_WEIGHTS_DOWN, -1, fake, fake), B.EB_ERR_INVALID_ARG),   # n < 0
+                       ((B.EB_WEIGHTS_DOWN, 1, None, fake), B.EB_ERR_INVALID_ARG),    # NULL
+                       ((B.EB_WEIGHTS_GATE_UP, 1, fake, fake + gu_bytes - 2), B.EB_ERR_INVALID_ARG),  # overlap
+                       ((B.EB_WEIGHTS_GATE_UP, 1, fake + 8, fake + 2 * gu_bytes), B.EB_ERR_INVALID_ARG)]:  # align
+        with pytest.raises(B.EasyBalanceError) as ei:
+            B.easybalance_pack_weights(d, *args)
+        assert ei.value.code == code, args
+    big = B.make_desc(2, 16384, 32768, 8, 2, 0, 4, "bf16")  # a gate/up matrix of 2 GiB
+    with pytest.raises(B.EasyBalanceError) as ei:
+        B.easybalance_pack_weights(big, B.EB_WEIGHTS_GATE_UP, 1, fake, fake * 4096)
+    assert ei.value.code == B.EB_ERR_UNSUPPORTED

@@ -19,7 +19,7 @@ from oracle.numerics import cast_fn
 from synth import CONFIGS, gen, mini
 from synth.device import DeviceInputs, fill_
 
-from gpu_helpers import assert_close, host_weights, log, make_stack, to_np
+from gpu_helpers import assert_close, ensure_packed, host_weights, log, make_stack, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -35,6 +35,54 @@ def _binding():
     from paper_2608_07964_amd import binding as B
     B.lib()
     return B
+
+
+def _pack_reference(W: np.ndarray, F: int, gateup: bool) -> np.ndarray:
+    """The packed layout as include/easybalance.h states it, for n matrices
+    W [n][N][K] of 16-bit patterns: block (s, t) = K columns 64 s .. of
+    column tile t, block row r = a weight row (gate/up rows interleaved per
+    64), chunk c = the 8 columns of logical chunk c ^ ((r >> 1) & 7)."""
+    n, N, K = W.shape
+    r = np.arange(256)
+    out = np.empty((n, K // 64, N // 256, 256, 8, 8), dtype=W.dtype)
+    for t in range(N // 256):
+        if gateup:
+            q = r % 64
+            rows = 128 * t + 32 * (r // 64) + np.where(q < 32, q, q - 32 + F)
+        else:
+            rows = 256 * t + r
+        for s in range(K // 64):
+            for c in range(8):
+                cols = 64 * s + 8 * (c ^ ((r >> 1) & 7))[:, None] + np.arange(8)[None, :]
+                out[:, s, t, :, c, :] = W[:, rows[:, None], cols]
+    return out.reshape(n, N * K)
+
+
+def test_pack_weights_layout(device):
+    """easybalance_pack_weights: every element of the packed bf16 gate/up and
+    down matrices of three experts sits where the documented layout puts it
+    (bit-exact, random bit patterns); fp32 packing is a copy."""
+    B = _binding()
+    for H, F in ((512, 384), (256, 128)):
+        log(f"pack layout H={H} F={F}")
+        desc = B.make_desc(1, H, F, 8, 2, 0, 4, "bf16")
+        g = torch.Generator(device="cpu").manual_seed(H + F)
+        for kind, N, K in ((B.EB_WEIGHTS_GATE_UP, 2 * F, H), (B.EB_WEIGHTS_DOWN, H, F)):
+            bits = torch.randint(-32768, 32768, (3, N, K), generator=g, dtype=torch.int32).to(torch.int16)
+            src = bits.to(device).view(torch.bfloat16)
+            dst = torch.empty_like(src)
+            B.easybalance_pack_weights(desc, kind, 3, src, dst)
+            torch.cuda.synchronize()
+            got = dst.view(torch.int16).cpu().numpy().reshape(3, N * K)
+            ref = _pack_reference(bits.numpy(), F, kind == B.EB_WEIGHTS_GATE_UP)
+            assert np.array_equal(got, ref), (H, F, kind)
+            assert torch.equal(src.view(torch.int16).cpu(), bits)  # src untouched
+    d32 = B.make_desc(1, 256, 128, 8, 2, 0, 4, "f32")
+    src = torch.randn(2, 256, 128, device=device)
+    dst = torch.empty_like(src)
+    B.easybalance_pack_weights(d32, B.EB_WEIGHTS_DOWN, 2, src, dst)
+    torch.cuda.synchronize()
+    assert torch.equal(dst, src)
 
 
 def test_device_generator_bit_exact(device):
@@ -97,7 +145,7 @@ def test_moe_step_and_combine_stage(cfg, device):
     token counts; every stage checked against the oracle on the GPU's inputs."""
     B = _binding()
     log(f"step parity {cfg.name}")
-    inp = DeviceInputs(cfg, device)
+    inp = ensure_packed(cfg, DeviceInputs(cfg, device))
     P = host_weights(cfg)
     cast = cast_fn(cfg.dtype)
     desc = B.make_desc(cfg.L, cfg.H, cfg.F, cfg.E, cfg.k, cfg.S, cfg.D, cfg.dtype, cfg.eps)
@@ -231,7 +279,7 @@ def test_moe_step_group_sizes_span_tile_shapes(device):
     cfg = mini(CONFIGS[1], H=256, F=256, L=3)
     assert cfg.k == 2 and cfg.E == 8 and cfg.S == 0
     log(f"group-size parity {cfg.name}")
-    inp = DeviceInputs(cfg, device)
+    inp = ensure_packed(cfg, DeviceInputs(cfg, device))
     P = host_weights(cfg)
     cast = cast_fn(cfg.dtype)
     desc = B.make_desc(cfg.L, cfg.H, cfg.F, cfg.E, cfg.k, cfg.S, cfg.D, cfg.dtype, cfg.eps)
