@@ -307,8 +307,10 @@ int easybalance_run_pass(const eb_model_desc* desc, int32_t N, int32_t T, float*
  * easybalance_profile_end(), every kernel the library launches whose class
  * EB_K_* has its bit (1u << EB_K_*) set in kernel_mask is bracketed by HIP
  * events recorded on the stream it is launched on (EB_PROFILE_ALL selects
- * every class; each event pair adds a little time to the stream, so a caller
- * timing a whole pass selects only the kernels it needs).  profile_end waits
+ * every class).  The events only time: they are recorded without a
+ * system-scope fence, so they do not order memory for the host; each pair
+ * still adds a little time to the stream, so a caller timing a whole pass
+ * selects only the kernels it needs.  profile_end waits
  * for those events and returns, per kernel class, the summed duration in ms
  * (ms_out[EB_NUM_KERNELS]) and the launch count (launches_out[EB_NUM_KERNELS]);
  * both host arrays are nullable.  Process-wide state, guarded by a mutex.

@@ -163,8 +163,10 @@ hipEvent_t prof_event() {
     g_prof_free.pop_back();
     return e;
   }
+  // timing only: no system-scope fence (cache writeback and invalidate) when
+  // the event is recorded, which would stall the kernels around it
   hipEvent_t e = nullptr;
-  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
   return e;
 }
 
