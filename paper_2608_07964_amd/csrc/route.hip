@@ -162,8 +162,9 @@ __device__ __forceinline__ void topk_token(int E, int k, int norm_topk, ZRow zro
 // % 8): lane sub holds the logits e = sub + 8 i (i < PER) and each pick is an
 // argmax over the 8 lanes' local bests under the same total order; the
 // softmax maximum and denominator are reduced over the 8 lanes in a fixed
-// pattern.  Lane sub 0 writes idx_t and w_t.
-template <int PER>
+// pattern.  The picks stay in registers (k <= KMAX) and lane sub 0 writes
+// idx_t and w_t once.
+template <int PER, int KMAX>
 __device__ __forceinline__ void topk_group8(int sub, int E, int k, int norm_topk, const float* zrow,
                                             int32_t* __restrict__ idx_t, float* __restrict__ w_t) {
   static_assert(PER <= 32, "taken mask");
@@ -190,38 +191,48 @@ __device__ __forceinline__ void topk_group8(int sub, int E, int k, int norm_topk
 #pragma unroll
   for (int off = 1; off < 8; off <<= 1) se += __shfl_xor(se, off, 8);
   float esum = 0.f;
-  for (int r = 0; r < k; ++r) {
-    float bv = -INFINITY;
-    int be = E;  // sentinel: nothing selectable in this lane
+  float pw[KMAX];
+  int pe[KMAX];
 #pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int e = sub + 8 * i;
-      if (!(taken & (1u << i)) && better(v[i], e, bv, be)) {
-        bv = v[i];
-        be = e;
-      }
-    }
+  for (int r = 0; r < KMAX; ++r) {
+    pw[r] = 0.f;
+    pe[r] = 0;
+    if (r < k) {
+      float bv = -INFINITY;
+      int be = E;  // sentinel: nothing selectable in this lane
 #pragma unroll
-    for (int off = 1; off < 8; off <<= 1) {
-      const float ov = __shfl_xor(bv, off, 8);
-      const int oe = __shfl_xor(be, off, 8);
-      if (better(ov, oe, bv, be)) {
-        bv = ov;
-        be = oe;
+      for (int i = 0; i < PER; ++i) {
+        const int e = sub + 8 * i;
+        if (!(taken & (1u << i)) && better(v[i], e, bv, be)) {
+          bv = v[i];
+          be = e;
+        }
       }
-    }
-    if (be >= E) be = E - 1;  // only when every remaining logit is NaN
-    if ((be & 7) == sub) taken |= 1u << (be >> 3);
-    const float ev = expf(bv - mx);
-    esum += ev;
-    if (sub == 0) {
-      idx_t[r] = be;
-      w_t[r] = ev;
+#pragma unroll
+      for (int off = 1; off < 8; off <<= 1) {
+        const float ov = __shfl_xor(bv, off, 8);
+        const int oe = __shfl_xor(be, off, 8);
+        if (better(ov, oe, bv, be)) {
+          bv = ov;
+          be = oe;
+        }
+      }
+      if (be >= E) be = E - 1;  // only when every remaining logit is NaN
+      if ((be & 7) == sub) taken |= 1u << (be >> 3);
+      const float ev = expf(bv - mx);
+      esum += ev;
+      pw[r] = ev;
+      pe[r] = be;
     }
   }
   if (sub == 0) {
     const float denom = norm_topk ? esum : se;
-    for (int r = 0; r < k; ++r) w_t[r] = w_t[r] / denom;
+#pragma unroll
+    for (int r = 0; r < KMAX; ++r)
+      if (r < k) {
+        idx_t[r] = pe[r];
+        w_t[r] = pw[r] / denom;
+      }
   }
 }
 
@@ -530,9 +541,14 @@ __global__ __launch_bounds__(256) void route_mfma_kernel(RouteBatch rb, int H, i
   __syncthreads();
   // 8 lanes per token
   const int tl = threadIdx.x >> 3, t = t0 + tl;
-  if (t < T)
-    topk_group8<NB * 4>(threadIdx.x & 7, E, k, norm_topk, zs[tl], idx + (size_t)t * k,
-                        w + (size_t)t * k);
+  if (t < T) {
+    if (k <= 8)
+      topk_group8<NB * 4, 8>(threadIdx.x & 7, E, k, norm_topk, zs[tl], idx + (size_t)t * k,
+                             w + (size_t)t * k);
+    else
+      topk_group8<NB * 4, 16>(threadIdx.x & 7, E, k, norm_topk, zs[tl], idx + (size_t)t * k,
+                              w + (size_t)t * k);
+  }
 }
 
 // ---------------------------------------------------------------------------
