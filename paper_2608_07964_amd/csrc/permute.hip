@@ -14,6 +14,9 @@
 //                        per-wavefront 64-bit expert masks (popcount of the lanes
 //                        below), then inv and perm
 //   gather_rows_kernel   one wavefront per grouped row: a_perm[p] = a of perm[p]
+//   gather_tokens_kernel (many pairs of long rows) one wavefront per (token,
+//                        2 KB piece of its row): the piece, read once, to
+//                        a_perm[inv[q]] for each of the token's k+S pairs q
 //
 // Pair q = (tok_base[rho] + t) * (k+S) + r; key = layer*(E+S) + slot expert.
 // All results are integers fixed by the inputs (no order-dependent atomics).
@@ -236,6 +239,8 @@ __global__ __launch_bounds__(kPermChunk) void perm_scatter_kernel(
   }
 }
 
+// One wavefront per grouped row: a_perm[p] = a of perm[p].  A token's row is
+// read once per pair; used when a token has few pairs or short rows.
 __global__ __launch_bounds__(256) void gather_rows_kernel(RunTable rt, int P, int elem_bytes,
                                                           const int32_t* __restrict__ perm,
                                                           uint8_t* __restrict__ a_perm) {
@@ -251,6 +256,46 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(RunTable rt, int P, in
   uint4* dst = reinterpret_cast<uint4*>(a_perm + (size_t)p * row_bytes);
   const int n16 = (int)(row_bytes / 16);
   for (int c = lane; c < n16; c += 64) dst[c] = src[c];
+}
+
+// One wavefront per (token, 2 KB piece of its row): the piece is read once
+// (two 16-byte loads per lane) and written to the grouped positions inv[q]
+// of all the token's k+S pairs.
+constexpr int kGatherU = 2;                  // 16-byte loads per lane per piece
+constexpr int kGatherPiece = 64 * kGatherU;  // 16-byte chunks per piece
+
+__global__ __launch_bounds__(256) void gather_tokens_kernel(RunTable rt, int total, int pieces,
+                                                          int elem_bytes,
+                                                          const int32_t* __restrict__ inv,
+                                                          uint8_t* __restrict__ a_perm) {
+  const int lane = threadIdx.x & 63;
+  const long long wv = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (wv >= (long long)total * pieces) return;
+  const int g = (int)(wv / pieces);  // global token of the step
+  const int c0 = (int)(wv - (long long)g * pieces) * kGatherPiece;
+  const int slots = rt.k + rt.S;
+  const int P = total * slots;
+  const int rho = find_entry(rt.tok_base, rt.n, g);
+  const int t = g - rt.tok_base[rho];
+  const size_t row_bytes = (size_t)rt.H * elem_bytes;
+  const uint4* src = reinterpret_cast<const uint4*>(static_cast<const uint8_t*>(rt.a[rho]) + (size_t)t * row_bytes);
+  // lane r < slots holds the grouped position of slot r (clamped into range)
+  const int pos = lane < slots ? min(max(inv[(size_t)g * slots + lane], 0), P - 1) : 0;
+  const int n16 = (int)(row_bytes / 16);
+  uint4 v[kGatherU];
+#pragma unroll
+  for (int j = 0; j < kGatherU; ++j) {
+    const int c = c0 + 64 * j + lane;
+    if (c < n16) v[j] = src[c];
+  }
+  for (int r = 0; r < slots; ++r) {
+    uint4* dst = reinterpret_cast<uint4*>(a_perm + (size_t)__shfl(pos, r, 64) * row_bytes);
+#pragma unroll
+    for (int j = 0; j < kGatherU; ++j) {
+      const int c = c0 + 64 * j + lane;
+      if (c < n16) dst[c] = v[j];
+    }
+  }
 }
 
 }  // namespace
@@ -283,9 +328,23 @@ hipError_t launch_perm_scatter(const RunTable& rt, int n_chunks, int P, int elem
   hipLaunchKernelGGL(perm_scatter_kernel, dim3(n_chunks), dim3(kPermChunk), 0, s, rt, chunk_base,
                      perm, inv);
   prof_stop(EB_K_PERM_SCATTER, s);
+  // read each token's row once when that saves >= 32 KB of re-reads per
+  // token (many pairs of long rows: the DeepSeek-V3 shape); else one
+  // wavefront per grouped row, which keeps more wavefronts in flight
+  const int slots = rt.k + rt.S;
+  const size_t row_bytes = (size_t)rt.H * elem_bytes;
   prof_start(EB_K_PERM_GATHER, s);
-  hipLaunchKernelGGL(gather_rows_kernel, dim3((P + 3) / 4), dim3(256), 0, s, rt, P, elem_bytes, perm,
-                     static_cast<uint8_t*>(a_perm));
+  if ((size_t)(slots - 1) * row_bytes >= 32768) {
+    const int total = P / slots;
+    const int n16 = (int)(row_bytes / 16);
+    const int pieces = (n16 + kGatherPiece - 1) / kGatherPiece;
+    const long long waves = (long long)total * pieces;
+    hipLaunchKernelGGL(gather_tokens_kernel, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s, rt,
+                       total, pieces, elem_bytes, inv, static_cast<uint8_t*>(a_perm));
+  } else {
+    hipLaunchKernelGGL(gather_rows_kernel, dim3((P + 3) / 4), dim3(256), 0, s, rt, P, elem_bytes, perm,
+                       static_cast<uint8_t*>(a_perm));
+  }
   prof_stop(EB_K_PERM_GATHER, s);
   return hipGetLastError();
 }

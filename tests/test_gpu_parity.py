@@ -27,8 +27,11 @@ MINIS = [CONFIGS[0]] + [mini(c) for c in CONFIGS[1:]]
 IDS = [c.name for c in MINIS]
 # long K (F >= 8192): the down GEMM runs its two K halves as separate items
 LONGK = mini(CONFIGS[1], H=256, F=8192, T=96, L=2)
-STEP_CFGS = MINIS + [LONGK]
-STEP_IDS = IDS + [LONGK.name + "_longk"]
+# many pairs of long rows ((k+S-1) * H * 2 >= 32 KB): the grouping reads each
+# token's row once (gather_tokens_kernel)
+ROWONCE = mini(CONFIGS[4], H=2048, T=96, L=2)
+STEP_CFGS = MINIS + [LONGK, ROWONCE]
+STEP_IDS = IDS + [LONGK.name + "_longk", ROWONCE.name + "_rowonce"]
 
 
 def _binding():
