@@ -6,14 +6,14 @@ import numpy as np
 import pytest
 import torch
 
-from synth import CONFIGS, mini
+from synth import BY_NAME, CONFIGS, mini
 from synth.device import DeviceInputs
 
 from gpu_helpers import log, make_stack
 
 pytestmark = pytest.mark.gpu
 
-SMALL = [CONFIGS[0]] + [mini(c) for c in CONFIGS[1:]] + [mini(CONFIGS[1], H=256, F=8192, T=96, L=2)]
+SMALL = [c if c.dtype == "f32" else mini(c) for c in CONFIGS] + [mini(BY_NAME["mixtral_bf16"], H=256, F=8192, T=96, L=2)]
 SMALL_IDS = [c.name for c in SMALL[:-1]] + [SMALL[-1].name + "_longk"]
 
 

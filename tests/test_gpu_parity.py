@@ -16,20 +16,20 @@ from oracle import model as omodel
 from oracle import permute as operm
 from oracle import sched as osched
 from oracle.numerics import cast_fn
-from synth import CONFIGS, gen, mini
+from synth import BY_NAME, CONFIGS, gen, mini
 from synth.device import DeviceInputs, fill_
 
 from gpu_helpers import assert_close, ensure_packed, host_weights, log, make_stack, to_np
 
 pytestmark = pytest.mark.gpu
 
-MINIS = [CONFIGS[0]] + [mini(c) for c in CONFIGS[1:]]
+MINIS = [c if c.dtype == "f32" else mini(c) for c in CONFIGS]
 IDS = [c.name for c in MINIS]
 # long K (F >= 8192): the down GEMM runs its two K halves as separate items
-LONGK = mini(CONFIGS[1], H=256, F=8192, T=96, L=2)
+LONGK = mini(BY_NAME["mixtral_bf16"], H=256, F=8192, T=96, L=2)
 # many pairs of long rows ((k+S-1) * H * 2 >= 32 KB): the grouping reads each
 # token's row once (gather_tokens_kernel)
-ROWONCE = mini(CONFIGS[4], H=2048, T=96, L=2)
+ROWONCE = mini(BY_NAME["dsv3_share_bf16"], H=2048, T=96, L=2)
 STEP_CFGS = MINIS + [LONGK, ROWONCE]
 STEP_IDS = IDS + [LONGK.name + "_longk", ROWONCE.name + "_rowonce"]
 
@@ -218,7 +218,7 @@ def test_moe_step_and_combine_stage(cfg, device):
 def test_tiny_fp32_end_to_end_free_running(device):
     """The fp32 stack through the whole EB pass against the oracle's plain
     layer-by-layer run: routing, schedule and hidden states."""
-    cfg = CONFIGS[0]
+    cfg = BY_NAME["tiny_f32"]
     log("end-to-end tiny fp32")
     st, inp = make_stack(cfg, device)
     steps = st.run("maxutil", m=cfg.m)
@@ -279,7 +279,7 @@ def test_moe_step_group_sizes_span_tile_shapes(device):
     whose (layer, expert) groups take every row count around the tile-shape
     boundaries; every row of h and o checked against the oracle."""
     B = _binding()
-    cfg = mini(CONFIGS[1], H=256, F=256, L=3)
+    cfg = mini(BY_NAME["mixtral_bf16"], H=256, F=256, L=3)
     assert cfg.k == 2 and cfg.E == 8 and cfg.S == 0
     log(f"group-size parity {cfg.name}")
     inp = ensure_packed(cfg, DeviceInputs(cfg, device))

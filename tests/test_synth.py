@@ -2,7 +2,7 @@
 import numpy as np
 import torch
 
-from synth import CONFIGS, gen, mini
+from synth import BY_NAME, CONFIGS, gen, mini
 
 
 def test_mix64_reference_values():
@@ -26,7 +26,7 @@ def test_numpy_stream_matches_scalar_definition():
 
 
 def test_slices_are_consistent():
-    cfg = mini(CONFIGS[2])
+    cfg = mini(BY_NAME["qwen_moe_bf16"])
     gate, up = gen.expert_gate_up(cfg, 1, 5)
     full = gen.tensor_values(cfg, gen.KIND_GU, 1, 0, (cfg.E + cfg.S) * 2 * cfg.F * cfg.H)
     full = full.reshape(cfg.E + cfg.S, 2 * cfg.F, cfg.H)
@@ -61,7 +61,7 @@ def test_router_bias_skew_models():
             zipf /= zipf.sum()
             assert np.allclose(np.sort(p, axis=1)[:, ::-1], zipf[None], rtol=1e-5)
     # drift: hot experts persist between consecutive layers
-    cfg = CONFIGS[4]
+    cfg = BY_NAME["dsv3_share_bf16"]
     b = gen.router_bias(cfg)
     top = [set(np.argsort(-b[l])[:16]) for l in range(cfg.L)]
     assert all(len(top[l] & top[l + 1]) >= 8 for l in range(cfg.L - 1))
