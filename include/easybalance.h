@@ -237,7 +237,8 @@ int easybalance_moe_step(const eb_model_desc* desc, int32_t n_run, const eb_work
  *   its 16-byte chunk at position c holds K columns 64s + 8(c ^ ((r>>1)&7))
  *   .. +7.  fp32: dst is a copy of src (row-major).
  * Enqueued on `stream`; errors: EB_ERR_INVALID_ARG (bad kind, n < 0, NULL,
- * overlap, misalignment), EB_ERR_HIP.
+ * overlap, misalignment), EB_ERR_UNSUPPORTED (descriptor outside the shape
+ * limits above), EB_ERR_HIP.
  */
 int easybalance_pack_weights(const eb_model_desc* desc, int32_t kind, int32_t n, const void* src,
                              void* dst, void* stream);
