@@ -57,6 +57,26 @@ def test_schedule_matches_oracle_bit_exact(policy):
         assert np.array_equal(load, sum(loads[j] for j in want))
 
 
+def test_maxutil_large_pools_match_oracle():
+    """Pools of 13-16 micro-batches with m from n - 4 to n (the candidate sets
+    are the complements of at most 4 excluded ones), small count ranges (many
+    ties) and counts near 2^31 (the exact 128-bit comparison decides)."""
+    rng = np.random.default_rng(34)
+    for trial in range(8):
+        n = int(rng.integers(13, 17))
+        D, per = int(rng.choice([4, 8])), 2
+        E = D * per
+        m = int(rng.integers(n - 4, n + 1))
+        ids = sorted(rng.choice(64, size=n, replace=False).tolist())
+        hi = [3, 1000, 2 ** 31 - 1][trial % 3]
+        counts = rng.integers(0, hi, size=(n, E)).astype(np.int32)
+        mask, load = B.easybalance_schedule(ids, counts, E, D, m, B.EB_POLICY_MAXUTIL)
+        loads = {j: omodel.device_loads(counts[i], D) for i, j in enumerate(ids)}
+        want = osched.schedule(ids, loads, D, m, osched.MAXUTIL)
+        assert tuple(j for j in ids if (mask >> j) & 1) == want, (n, m, hi)
+        assert np.array_equal(load, sum(loads[j] for j in want))
+
+
 def test_schedule_large_pool_and_overflow_safety():
     # 16 micro-batches (the decode-like stack) and counts near 2^31
     rng = np.random.default_rng(33)
