@@ -133,3 +133,19 @@ def test_placed_loads_split_and_contiguous_case():
     placements = [sweep.replicated_placement(counts.sum(axis=0)[l], 4, 4, l) for l in range(3)]
     w = sweep.placed_loads(counts, placements)
     assert np.array_equal(w.sum(axis=2), counts.sum(axis=2))  # pairs are conserved
+
+
+def test_report_sections_on_synthetic_routes():
+    # the markdown report of a small stack: every section present, the
+    # placement rows for E and E + D physical experts with both tie orders
+    from synth import mini, BY_NAME
+    cfg = mini(BY_NAME["qwen_moe_bf16"], T=32, L=3)
+    rng = np.random.default_rng(11)
+    r = _routes(rng, cfg.N * cfg.T, cfg.L, cfg.k, cfg.E)
+    rep = sweep.report(r, cfg)
+    for head in ("Policies (N =", "MaxUtil over N and m", "Virtual devices D", "Static placement + EasyBalance",
+                 "Host time per scheduling decision", "Windows of n consecutive layers"):
+        assert head in rep, head
+    for phys in (cfg.E, cfg.E + cfg.D):
+        for ties in ("ties at device 0", "ties rotated by layer"):
+            assert f"placed from history, {phys} physical experts, {ties}" in rep
