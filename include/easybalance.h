@@ -213,6 +213,9 @@ int easybalance_moe_step_workspace_size(const eb_model_desc* desc, int32_t n_run
  * inv_out  device [P] int32: grouped position of pair q
  * views    host pointer to optional outputs (nullable)
  * Expert ids outside [0, E) in idx are clamped into range (no fault).
+ * A step whose entries all have T = 0 (P = 0) enqueues nothing and writes
+ * no output, views->offsets included; the weight and output pointers are
+ * then not checked.
  */
 int easybalance_moe_step(const eb_model_desc* desc, int32_t n_run, const eb_work* run,
                          const void* const* W_gu, const void* const* W_dn, void* ws,

@@ -188,3 +188,17 @@ def test_pack_weights_rejects_bad_arguments_before_touching_the_gpu():
     with pytest.raises(B.EasyBalanceError) as ei:
         B.easybalance_pack_weights(big, B.EB_WEIGHTS_GATE_UP, 1, fake, fake * 4096)
     assert ei.value.code == B.EB_ERR_UNSUPPORTED
+
+
+def test_empty_step_enqueues_nothing():
+    """A step whose entries all have T = 0 returns before any HIP call: no
+    pointer is dereferenced or checked, so NULL weights and outputs pass."""
+    d = B.make_desc(2, 256, 128, 8, 2, 0, 4, "bf16")
+    run = B.work_array([(0, 0, 0, None, None, None), (1, 1, 0, None, None, None)])
+    assert B.easybalance_moe_step_workspace_size(d, [0, 0]) >= 0
+    B.easybalance_moe_step(d, run, 2, [None, None], [None, None], None, 0, None, None)
+    B.easybalance_combine(d, run, 2, [None, None], None, None)
+    bad = B.work_array([(0, 2, 0, None, None, None)])   # layer outside [0, L) is still rejected
+    with pytest.raises(B.EasyBalanceError) as ei:
+        B.easybalance_moe_step(d, bad, 1, [None, None], [None, None], None, 0, None, None)
+    assert ei.value.code == B.EB_ERR_INVALID_ARG
