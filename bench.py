@@ -111,6 +111,10 @@ def main() -> int:
     ap.add_argument("--config", default="mixtral_bf16")
     ap.add_argument("--policy", default="maxutil", choices=["maxutil", "cumutil", "diffpeak", "lockstep"])
     ap.add_argument("--m", type=int, default=None, help="minimum combination size (default 0.75 N)")
+    ap.add_argument("--schedule", default="host", choices=["host", "device"],
+                    help="where Algorithm 1's Schedule runs: on the host after a copy of the pool's "
+                         "expert counts each step, or in a kernel on the GPU with the host queueing "
+                         "steps ahead")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-lockstep", action="store_true", help="skip the lock-step comparison pass")
@@ -154,7 +158,8 @@ def main() -> int:
     def one_pass(policy, record=False):
         # one Algorithm-1 pass through the library's native driver
         st.x.copy_(inp.x0)
-        return st.run_native(policy, m=m, record=record, stream=stream)
+        return st.run_native(policy, m=m, record=record, stream=stream,
+                             device_schedule=args.schedule == "device")
 
     flop_pass = cfg.total_ffn_flop
     pairs_pass = cfg.N * cfg.T * (cfg.k + cfg.S) * cfg.L
@@ -235,6 +240,7 @@ def main() -> int:
         "dtype": "bf16" if cfg.dtype == "bf16" else "f32", "data": "synthetic",
         "config": {"workload": cfg.name, "L": cfg.L, "H": cfg.H, "F": cfg.F, "E": cfg.E, "k": cfg.k,
                    "S": cfg.S, "D": cfg.D, "N": cfg.N, "T": cfg.T, "m": m, "policy": args.policy,
+                   "schedule": args.schedule,
                    "tokens_per_step": cfg.N * cfg.T, "ffn_flop_per_step": flop_pass},
         "load": load,
         "steps_per_pass": len(steps),

@@ -59,6 +59,8 @@ extern "C" {
 
 #define EB_POLICY_LOCKSTEP 3    /* easybalance_run_pass only: every pooled
                                    micro-batch every step (per-layer baseline) */
+#define EB_PASS_DEVICE_SCHEDULE 0x100  /* easybalance_run_pass only, OR-ed into
+                                   policy: Schedule runs on the GPU */
 
 #define EB_MAX_POOL 64          /* micro-batch ids are 0..63 (one bit each)   */
 #define EB_MAXUTIL_MAX_POOL 20  /* MaxUtil enumerates up to 2^n subsets       */
@@ -274,6 +276,16 @@ int easybalance_combine(const eb_model_desc* desc, int32_t n_run, const eb_work*
  * The results are the ones the same sequence of calls through the other entry
  * points gives.  The only host<->device synchronisation per step is the copy
  * of the pool's expert counts to pinned host memory for the scheduler.
+ *
+ * policy | EB_PASS_DEVICE_SCHEDULE: the same pass with Schedule on the GPU (a
+ * one-workgroup kernel at the start of each step, exact integer arithmetic,
+ * the same RunSets bit for bit), every step's kernels reading their tables
+ * from device memory, and the host queueing steps ahead instead of waiting
+ * for the counts: it queues only steps that must run (s steps done and a
+ * micro-batch L - l layers short need s + L - l in all) and reads a status
+ * word the scheduler kernel writes to host-mapped memory.  The call returns
+ * once the last step is queued (after the records are copied, if any are
+ * asked for).  EB_ERR_UNSUPPORTED if D > 64 or, for fp32, E > 64.
  *
  * x            device [N][T][H] fp32, updated in place (the residual stream)
  * gain         device [L][H] fp32;  bias  device [L][E] fp32

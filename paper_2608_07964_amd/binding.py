@@ -23,6 +23,7 @@ EB_ERR_HIP = -3
 EB_ERR_WORKSPACE_TOO_SMALL = -4
 EB_DTYPE_F32, EB_DTYPE_BF16 = 0, 1
 EB_POLICY_MAXUTIL, EB_POLICY_CUMUTIL, EB_POLICY_DIFFPEAK, EB_POLICY_LOCKSTEP = 0, 1, 2, 3
+EB_PASS_DEVICE_SCHEDULE = 0x100  # OR-ed into easybalance_run_pass's policy
 EB_WEIGHTS_GATE_UP, EB_WEIGHTS_DOWN = 0, 1
 EB_MAX_POOL = 64
 EB_MAXUTIL_MAX_POOL = 20

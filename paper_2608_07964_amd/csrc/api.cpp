@@ -145,6 +145,65 @@ int hip_status(hipError_t e, const char* what) {
   return set_error(EB_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
+// A step's buffers carved from its workspace (laid out for shape sh); views
+// that the caller provides replace their workspace slots.
+struct StepWs {
+  StepBuffers b;
+  float* partial;
+  void* h;
+};
+
+StepWs carve_step(const eb_model_desc& d, const StepShape& sh, const eb_step_views* views, void* ws,
+                  int32_t* inv) {
+  const WsLayout L = ws_layout(d, sh, views);
+  uint8_t* base = static_cast<uint8_t*>(ws);
+  StepWs w;
+  StepBuffers& b = w.b;
+  b.hist = reinterpret_cast<int32_t*>(base + L.hist);
+  b.chunk_base = reinterpret_cast<int32_t*>(base + L.chunk_base);
+  b.offsets = (views && views->offsets) ? views->offsets : reinterpret_cast<int32_t*>(base + L.offsets);
+  b.tiles = reinterpret_cast<int4*>(base + L.tiles);
+  b.n_tiles = reinterpret_cast<int32_t*>(base + L.n_tiles);
+  b.groups = reinterpret_cast<int4*>(base + L.groups);
+  b.n_groups = reinterpret_cast<int32_t*>(base + L.n_groups);
+  b.work_ctr = reinterpret_cast<int32_t*>(base + L.work_ctr);
+  b.max_tiles = sh.max_tiles;
+  b.perm = (views && views->perm) ? views->perm : reinterpret_cast<int32_t*>(base + L.perm);
+  b.inv = inv;
+  b.a_perm = (views && views->a_perm) ? views->a_perm : base + L.a_perm;
+  w.partial = L.partial ? reinterpret_cast<float*>(base + L.partial) : nullptr;
+  w.h = (views && views->h) ? views->h : base + L.h;
+  return w;
+}
+
+// The two grouped GEMMs of a step whose permutation is queued before them.
+// sh.P rows are held by the buffers; the live rows come from the offsets.
+int run_gemms(const eb_model_desc& d, const StepShape& sh, const StepWs& w, const WeightTable& wt,
+              void* o, hipStream_t s) {
+  GroupedProblem gp;
+  gp.H = d.H;
+  gp.F = d.F;
+  gp.E = d.E;
+  gp.S = d.S;
+  gp.P = (int32_t)sh.P;
+  gp.offsets = w.b.offsets;
+  gp.P_live = w.b.offsets + (size_t)d.L * (d.E + d.S);
+  gp.tiles = w.b.tiles;
+  gp.n_tiles = w.b.n_tiles;
+  gp.groups = w.b.groups;
+  gp.n_groups = w.b.n_groups;
+  gp.max_tiles = sh.max_tiles;
+  gp.work_ctr = w.b.work_ctr;
+  gp.ksplit = 1;
+  gp.partial = nullptr;
+  int rc;
+  if ((rc = hip_status(launch_gateup(d.dtype, gp, wt, w.b.a_perm, w.h, s), "gate/up GEMM"))) return rc;
+  gp.work_ctr = w.b.work_ctr + kWorkCounters / 2;
+  gp.ksplit = down_ksplit(d.dtype, d.F);
+  gp.partial = w.partial;
+  return hip_status(launch_down(d.dtype, gp, wt, w.h, o, s), "down GEMM");
+}
+
 // ---- kernel timing ---------------------------------------------------------
 struct EventPair {
   hipEvent_t start, stop;
@@ -171,6 +230,21 @@ hipEvent_t prof_event() {
 }
 
 }  // namespace
+
+// One step of a device-scheduled pass: its run table is at rt (device
+// memory, written by the scheduler kernel queued before), its workspace laid
+// out for all N micro-batches of T tokens, every grid sized for that step.
+int enqueue_step_dev(const eb_model_desc& d, int N, int T, const RunTable* rt, const WeightTable& wt,
+                     void* ws, void* o, int32_t* inv, hipStream_t s) {
+  std::vector<int32_t> Ts(N, T);
+  const StepShape sh = step_shape(d, N, Ts.data());
+  const StepWs w = carve_step(d, sh, nullptr, ws, inv);
+  int rc;
+  if ((rc = hip_status(launch_permute_dev(d, rt, sh.n_chunks, (int)sh.tokens, w.b, s), "permute")))
+    return rc;
+  if ((rc = run_gemms(d, sh, w, wt, o, s))) return rc;
+  return hip_status(launch_combine_dev(rt, (int)sh.tokens, d.dtype, o, inv, s), "combine");
+}
 
 int set_error(int code, const char* fmt, ...) {
   va_list ap;
@@ -282,51 +356,21 @@ int easybalance_moe_step(const eb_model_desc* desc, int32_t n_run, const eb_work
   const WsLayout L = ws_layout(d, sh, views);
   if (ws_bytes < L.total)
     return set_error(EB_ERR_WORKSPACE_TOO_SMALL, "workspace %zu < %zu bytes", ws_bytes, L.total);
-  uint8_t* base = static_cast<uint8_t*>(ws);
-  int32_t* hist = reinterpret_cast<int32_t*>(base + L.hist);
-  int32_t* chunk_base = reinterpret_cast<int32_t*>(base + L.chunk_base);
-  int32_t* offsets = (views && views->offsets) ? views->offsets : reinterpret_cast<int32_t*>(base + L.offsets);
-  int4* tiles = reinterpret_cast<int4*>(base + L.tiles);
-  int32_t* n_tiles = reinterpret_cast<int32_t*>(base + L.n_tiles);
-  int4* groups = reinterpret_cast<int4*>(base + L.groups);
-  int32_t* n_groups = reinterpret_cast<int32_t*>(base + L.n_groups);
-  int32_t* work_ctr = reinterpret_cast<int32_t*>(base + L.work_ctr);
-  float* partial = L.partial ? reinterpret_cast<float*>(base + L.partial) : nullptr;
-  int32_t* perm = (views && views->perm) ? views->perm : reinterpret_cast<int32_t*>(base + L.perm);
-  void* a_perm = (views && views->a_perm) ? views->a_perm : base + L.a_perm;
-  void* h = (views && views->h) ? views->h : base + L.h;
+  const StepWs w = carve_step(d, sh, views, ws, inv_out);
   hipStream_t s = static_cast<hipStream_t>(stream);
 
   const RunTable rt = make_run_table(d, n_run, run, nullptr);
   const int eb = d.dtype == EB_DTYPE_BF16 ? 2 : 4;
-  if ((rc = hip_status(launch_perm_count(rt, sh.n_chunks, hist, s), "perm_count"))) return rc;
-  if ((rc = hip_status(launch_perm_scan(rt, sh.n_chunks, hist, chunk_base, offsets, tiles, n_tiles,
-                                        groups, n_groups, gemm_bm(d.dtype), sh.max_tiles, work_ctr, s),
+  const StepBuffers& b = w.b;
+  if ((rc = hip_status(launch_perm_count(rt, sh.n_chunks, b.hist, s), "perm_count"))) return rc;
+  if ((rc = hip_status(launch_perm_scan(rt, b.hist, b.chunk_base, b.offsets, b.tiles, b.n_tiles, b.groups,
+                                        b.n_groups, gemm_bm(d.dtype), b.max_tiles, b.work_ctr, s),
                        "perm_scan")))
     return rc;
-  if ((rc = hip_status(launch_perm_scatter(rt, sh.n_chunks, (int)sh.P, eb, chunk_base, perm, inv_out, a_perm, s),
+  if ((rc = hip_status(launch_perm_scatter(rt, sh.n_chunks, eb, b.chunk_base, b.perm, inv_out, b.a_perm, s),
                        "perm_scatter")))
     return rc;
-  GroupedProblem gp;
-  gp.H = d.H;
-  gp.F = d.F;
-  gp.E = d.E;
-  gp.S = d.S;
-  gp.P = (int32_t)sh.P;
-  gp.offsets = offsets;
-  gp.tiles = tiles;
-  gp.n_tiles = n_tiles;
-  gp.groups = groups;
-  gp.n_groups = n_groups;
-  gp.max_tiles = sh.max_tiles;
-  gp.work_ctr = work_ctr;
-  gp.ksplit = 1;
-  gp.partial = nullptr;
-  if ((rc = hip_status(launch_gateup(d.dtype, gp, wt, a_perm, h, s), "gate/up GEMM"))) return rc;
-  gp.work_ctr = work_ctr + kWorkCounters / 2;
-  gp.ksplit = down_ksplit(d.dtype, d.F);
-  gp.partial = partial;
-  return hip_status(launch_down(d.dtype, gp, wt, h, o_out, s), "down GEMM");
+  return run_gemms(d, sh, w, wt, o_out, s);
 }
 
 int easybalance_combine(const eb_model_desc* desc, int32_t n_run, const eb_work* run,
@@ -345,7 +389,7 @@ int easybalance_combine(const eb_model_desc* desc, int32_t n_run, const eb_work*
   if (tokens == 0) return EB_OK;
   if (o == nullptr || inv == nullptr) return set_error(EB_ERR_INVALID_ARG, "o/inv is NULL");
   const RunTable rt = make_run_table(*desc, n_run, run, x_inout);
-  return hip_status(launch_combine(rt, (int)tokens, desc->dtype, o, inv,
+  return hip_status(launch_combine(rt, desc->dtype, o, inv,
                                    static_cast<hipStream_t>(stream)),
                     "combine");
 }

@@ -40,13 +40,15 @@ struct Row8<bf16_t> {
   }
 };
 
-template <typename TO>
-__global__ __launch_bounds__(kCombThreads) void combine_kernel(RunTable rt, int total,
-                                                               const TO* __restrict__ o,
+template <typename TO, class RTA>
+__global__ __launch_bounds__(kCombThreads) void combine_kernel(RTA rta, const TO* __restrict__ o,
                                                                const int32_t* __restrict__ inv) {
   __shared__ int s_row[kMaxSlots];
   __shared__ float s_w[kMaxSlots];
+  const RunTable& rt = rta.get();
   const int g = blockIdx.x;
+  const int total = rt.tok_base[rt.n];
+  if (g >= total) return;  // past the live tokens (grid sized for the largest step)
   const int rho = find_entry(rt.tok_base, rt.n, g);
   const int t = g - rt.tok_base[rho];
   const int k = rt.k, slots = rt.k + rt.S, H = rt.H;
@@ -85,16 +87,33 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(RunTable rt, int 
 
 }  // namespace
 
-hipError_t launch_combine(const RunTable& rt, int total_tokens, int dtype, const void* o,
-                          const int32_t* inv, hipStream_t s) {
+namespace {
+
+template <class RTA>
+void combine_impl(RTA a, int grid_tokens, int dtype, const void* o, const int32_t* inv, hipStream_t s) {
   prof_start(EB_K_COMBINE, s);
-  if (dtype == EB_DTYPE_BF16)
-    hipLaunchKernelGGL(combine_kernel<bf16_t>, dim3(total_tokens), dim3(kCombThreads), 0, s, rt,
-                       total_tokens, static_cast<const bf16_t*>(o), inv);
-  else
-    hipLaunchKernelGGL(combine_kernel<float>, dim3(total_tokens), dim3(kCombThreads), 0, s, rt,
-                       total_tokens, static_cast<const float*>(o), inv);
+  if (grid_tokens > 0) {
+    if (dtype == EB_DTYPE_BF16)
+      hipLaunchKernelGGL((combine_kernel<bf16_t, RTA>), dim3(grid_tokens), dim3(kCombThreads), 0, s, a,
+                         static_cast<const bf16_t*>(o), inv);
+    else
+      hipLaunchKernelGGL((combine_kernel<float, RTA>), dim3(grid_tokens), dim3(kCombThreads), 0, s, a,
+                         static_cast<const float*>(o), inv);
+  }
   prof_stop(EB_K_COMBINE, s);
+}
+
+}  // namespace
+
+hipError_t launch_combine(const RunTable& rt, int dtype, const void* o, const int32_t* inv,
+                          hipStream_t s) {
+  combine_impl(ByValue<RunTable>{rt}, rt.tok_base[rt.n], dtype, o, inv, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_combine_dev(const RunTable* rt, int max_tokens, int dtype, const void* o,
+                              const int32_t* inv, hipStream_t s) {
+  combine_impl(InMemory<RunTable>{rt}, max_tokens, dtype, o, inv, s);
   return hipGetLastError();
 }
 

@@ -25,6 +25,21 @@ struct RunTable {
   float* x[EB_MAX_RUN];
 };
 
+// A kernel's view of a per-step table: in the kernel arguments (the host
+// built it) or in device memory (the device-side scheduler wrote it).  The
+// kernels take the live counts (entries, chunks, tokens) from the table
+// itself, so a grid sized for the largest step is cut to the live one.
+template <class Tab>
+struct ByValue {
+  Tab v;
+  __device__ __forceinline__ const Tab& get() const { return v; }
+};
+template <class Tab>
+struct InMemory {
+  const Tab* p;
+  __device__ __forceinline__ const Tab& get() const { return *p; }
+};
+
 // Per-layer expert weight tables, passed by value.
 struct WeightTable {
   const void* gu[EB_MAX_LAYERS];           // [E+S][2F][H]
@@ -34,8 +49,11 @@ struct WeightTable {
 // Grouped-GEMM problem of one step.
 struct GroupedProblem {
   int32_t H, F, E, S;                      // E+S expert slots per layer
-  int32_t P;                               // grouped rows
+  int32_t P;                               // grouped rows the buffers hold (the live
+                                           // rows or, device-scheduled, the largest step's)
   const int32_t* offsets;                  // [L*(E+S)+1]
+  const int32_t* P_live;                   // device scalar: the live grouped rows
+                                           // (offsets[L*(E+S)])
   const int4* tiles;                       // [n_tiles] the row block's group: (key, first row,
                                            // rows, index of the group's first row block)
   const int32_t* n_tiles;                  // device scalar: row blocks over all groups
@@ -85,20 +103,94 @@ struct RouteBatch {
   RouteEntry e[kRouteBatch];
 };
 
+// ---- device-scheduled pass --------------------------------------------------
+constexpr int kDevMaxD = 64;                       // virtual devices the device scheduler handles
+constexpr int kDevRouteSlots = (EB_MAX_POOL + kRouteBatch - 1) / kRouteBatch;
+constexpr int kDevMaxKeyWords = 15360 / 32;        // bitmap words over L * E <= 15360 keys
+
+// State of a device-scheduled pass, in device memory.
+struct DevPassState {
+  int32_t layer[EB_MAX_POOL];  // l_j; L once micro-batch j has finished
+  int32_t steps;               // steps scheduled so far
+};
+
+// Everything the scheduler kernel needs, by value.  Micro-batch j's buffers
+// sit at j * (its size) from each base: a (a_stride bytes), z [T][E],
+// idx / w [T][k], x [T][H] fp32, counts [E].
+struct DevPassArgs {
+  int32_t N, T, L, H, E, k, S, D, m, policy;
+  int32_t max_records;           // steps the record arrays hold (N * L)
+  int32_t tag;                   // pass tag echoed in the status word (16 bits)
+  void* a;
+  size_t a_stride;
+  float* z;
+  int32_t* idx;
+  float* w;
+  float* x;
+  int32_t* counts;
+  const float* gain;             // [L][H]
+  const float* bias;             // [L][E]
+  const void* Wg[EB_MAX_LAYERS]; // router weights of each layer
+  DevPassState* state;
+  RunTable* rt;                  // the step's run table
+  RouteBatch* rb;                // [kDevRouteSlots] routing after the step
+  uint64_t* rec_mask;            // [max_records] RunSet (bit j = micro-batch j)
+  int32_t* rec_layers;           // [max_records][N] layer of each member, -1 if not run
+  int64_t* rec_load;             // [max_records][D] the step's per-device workload
+  int32_t* rec_groups;           // [max_records] distinct (layer, expert) groups
+  int32_t* rec_layer_loads;      // [N][L][D] per-device load of (j, l), -1 until seen
+  unsigned long long* status;    // host-mapped: tag << 48 | steps << 16 | max_j (L - l_j)
+};
+
+hipError_t launch_pass_init(const DevPassArgs& A, hipStream_t s);
+hipError_t launch_sched_step(const DevPassArgs& A, hipStream_t s);
+// Permute, GEMMs and combine of one device-scheduled step (api.cpp);
+// returns EB_OK or an EB_ERR_* code.
+int enqueue_step_dev(const eb_model_desc& d, int N, int T, const RunTable* rt, const WeightTable& wt,
+                     void* ws, void* o, int32_t* inv, hipStream_t s);
+
 // ---- launchers (return hipError_t of the launch) ---------------------------
 hipError_t launch_route_batch(const eb_model_desc& d, const RouteBatch& rb, hipStream_t s);
+// A batch table in device memory (written by the device-side scheduler);
+// grids cover max_entries entries of T tokens.  Only for stacks whose
+// routing needs no launch per entry (route_batch_device_ok).
+bool route_batch_device_ok(const eb_model_desc& d);
+hipError_t launch_route_batch_dev(const eb_model_desc& d, const RouteBatch* rb, int max_entries, int T,
+                                  hipStream_t s);
 hipError_t launch_route(const eb_model_desc& d, int T, const float* x, const float* gain,
                         const void* Wg, const float* bias, void* a_out, float* logits,
                         int32_t* idx, float* w, int32_t* counts, hipStream_t s);
 
 hipError_t launch_perm_count(const RunTable& rt, int n_chunks, int32_t* hist, hipStream_t s);
-hipError_t launch_perm_scan(const RunTable& rt, int n_chunks, const int32_t* hist,
-                            int32_t* chunk_base, int32_t* offsets, int4* tiles,
-                            int32_t* n_tiles, int4* groups, int32_t* n_groups, int bm,
-                            int max_tiles, int32_t* work_ctr, hipStream_t s);
-hipError_t launch_perm_scatter(const RunTable& rt, int n_chunks, int P, int elem_bytes,
+hipError_t launch_perm_scan(const RunTable& rt, const int32_t* hist, int32_t* chunk_base,
+                            int32_t* offsets, int4* tiles, int32_t* n_tiles, int4* groups,
+                            int32_t* n_groups, int bm, int max_tiles, int32_t* work_ctr,
+                            hipStream_t s);
+hipError_t launch_perm_scatter(const RunTable& rt, int n_chunks, int elem_bytes,
                                const int32_t* chunk_base, int32_t* perm, int32_t* inv,
                                void* a_perm, hipStream_t s);
+
+// Workspace buffers of one step (see the workspace layout in api.cpp).
+struct StepBuffers {
+  int32_t* hist;
+  int32_t* chunk_base;
+  int32_t* offsets;
+  int4* tiles;
+  int32_t* n_tiles;
+  int4* groups;
+  int32_t* n_groups;
+  int32_t* work_ctr;
+  int32_t max_tiles;
+  int32_t* perm;
+  int32_t* inv;
+  void* a_perm;
+};
+
+// Count, scan, scatter and gather of a step whose run table a device-side
+// scheduler wrote to `rt` (device memory); grids cover max_chunks chunks and
+// max_tokens tokens, the largest step's.
+hipError_t launch_permute_dev(const eb_model_desc& d, const RunTable* rt, int max_chunks,
+                              int max_tokens, const StepBuffers& b, hipStream_t s);
 
 // Row-block height of the grouped GEMM tiles for a dtype.
 int gemm_bm(int dtype);
@@ -113,8 +205,10 @@ hipError_t launch_gateup(int dtype, const GroupedProblem& p, const WeightTable& 
 hipError_t launch_down(int dtype, const GroupedProblem& p, const WeightTable& wt,
                        const void* h, void* o, hipStream_t s);
 
-hipError_t launch_combine(const RunTable& rt, int total_tokens, int dtype, const void* o,
-                          const int32_t* inv, hipStream_t s);
+hipError_t launch_combine(const RunTable& rt, int dtype, const void* o, const int32_t* inv,
+                          hipStream_t s);
+hipError_t launch_combine_dev(const RunTable* rt, int max_tokens, int dtype, const void* o,
+                              const int32_t* inv, hipStream_t s);
 
 // Profiling hooks (api.cpp): bracket one launch of kernel class `kind`.
 void prof_start(int kind, hipStream_t s);

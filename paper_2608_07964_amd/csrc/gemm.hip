@@ -672,13 +672,15 @@ __global__ __launch_bounds__(256) void grouped_gemm_f32(GroupedProblem p, Weight
 }
 
 // o = dtype(p0 + p1) for the K halves of a split down GEMM, 4 elements per
-// thread (n = P*H is a multiple of 256).
-__global__ __launch_bounds__(256) void split_sum_kernel(const float* __restrict__ part, long long n,
+// thread over the live rows *P_live (H is a multiple of 256); the second
+// half starts `stride` floats after the first.
+__global__ __launch_bounds__(256) void split_sum_kernel(const float* __restrict__ part, long long stride,
+                                                        const int32_t* __restrict__ P_live, int H,
                                                         bf16_t* __restrict__ o) {
   const long long i = ((long long)blockIdx.x * blockDim.x + threadIdx.x) * 4;
-  if (i >= n) return;
+  if (i >= (long long)(*P_live) * H) return;
   const float4 a = *reinterpret_cast<const float4*>(part + i);
-  const float4 b = *reinterpret_cast<const float4*>(part + n + i);
+  const float4 b = *reinterpret_cast<const float4*>(part + stride + i);
   uint2 u;
   u.x = (uint32_t)f32_to_bf16(a.x + b.x) | ((uint32_t)f32_to_bf16(a.y + b.y) << 16);
   u.y = (uint32_t)f32_to_bf16(a.z + b.z) | ((uint32_t)f32_to_bf16(a.w + b.w) << 16);
@@ -774,7 +776,7 @@ hipError_t launch_down(int dtype, const GroupedProblem& p, const WeightTable& wt
     if (p.ksplit > 1) {
       const long long n = (long long)p.P * p.H;
       hipLaunchKernelGGL(split_sum_kernel, dim3((unsigned)((n / 4 + 255) / 256)), dim3(256), 0, s,
-                         p.partial, n, static_cast<bf16_t*>(o));
+                         p.partial, n, p.P_live, p.H, static_cast<bf16_t*>(o));
     }
   } else {
     hipLaunchKernelGGL(grouped_gemm_f32<MODE_DOWN>, dim3(p.max_tiles, p.H / FBN), dim3(256), 0, s,

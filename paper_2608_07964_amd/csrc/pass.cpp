@@ -7,13 +7,21 @@
 //     expert FFNs of RunSet jointly, then the combine      (MoECompute_Combine)
 //     l_j += 1 for j in RunSet; route those not finished
 //
-// The only host<->device synchronisation per step is the copy of the pool's
-// expert counts into pinned host memory that the scheduler needs; everything
-// else is queued on the caller's stream without waiting.
+// Host-scheduled, the only host<->device synchronisation per step is the
+// copy of the pool's expert counts into pinned host memory that the
+// scheduler needs; everything else is queued on the caller's stream without
+// waiting.  Device-scheduled (EB_PASS_DEVICE_SCHEDULE), a one-workgroup
+// kernel at the start of each step makes the same choice on the GPU and
+// writes the step's tables, and the host queues steps ahead of the GPU: it
+// never waits for the counts.  It queues only steps that must run: after s
+// steps with the furthest-behind micro-batch L - l layers short, at least
+// s + (L - l) steps are needed in all, and the scheduler kernel publishes
+// (s, L - l) in host memory as soon as it has chosen.
 #include <hip/hip_runtime.h>
 #include <string.h>
 
 #include <algorithm>
+#include <chrono>
 #include <vector>
 
 #include "eb_internal.h"
@@ -25,7 +33,10 @@ constexpr size_t kAlignP = 256;
 size_t align_p(size_t v) { return (v + kAlignP - 1) / kAlignP * kAlignP; }
 
 struct PassLayout {
-  size_t a, logits, idx, w, counts, o, inv, ws, ws_bytes, total;
+  size_t a, logits, idx, w, counts, o, inv, ws, ws_bytes;
+  // device-scheduled pass: scheduler state, step tables, records (N * L steps)
+  size_t dstate, drt, drb, rec_mask, rec_layers, rec_load, rec_groups, rec_ll;
+  size_t total;
 };
 
 PassLayout pass_layout(const eb_model_desc& d, int N, int T) {
@@ -50,6 +61,15 @@ PassLayout pass_layout(const eb_model_desc& d, int N, int T) {
   easybalance_moe_step_workspace_size(&d, N, Ts.data(), &wsb);
   p.ws_bytes = wsb;
   p.ws = take(wsb);
+  const size_t steps = (size_t)N * d.L;  // every step advances a micro-batch by a layer
+  p.dstate = take(sizeof(DevPassState));
+  p.drt = take(sizeof(RunTable));
+  p.drb = take(sizeof(RouteBatch) * kDevRouteSlots);
+  p.rec_mask = take(sizeof(uint64_t) * steps);
+  p.rec_layers = take(sizeof(int32_t) * steps * N);
+  p.rec_load = take(sizeof(int64_t) * steps * d.D);
+  p.rec_groups = take(sizeof(int32_t) * steps);
+  p.rec_ll = take(sizeof(int32_t) * (size_t)N * d.L * d.D);
   p.total = off;
   return p;
 }
@@ -74,6 +94,167 @@ struct PinnedCounts {
   }
 };
 thread_local PinnedCounts t_pinned;
+
+// Host-mapped status word of device-scheduled passes, one per host thread;
+// the tag tells this pass's words from an earlier pass's.
+struct PinnedStatus {
+  unsigned long long* h = nullptr;
+  unsigned long long* d = nullptr;
+  uint32_t tag = 0;
+  ~PinnedStatus() {
+    if (h) (void)hipHostFree(h);
+  }
+  bool ready() {
+    if (h) return true;
+    void* p = nullptr;
+    if (hipHostMalloc(&p, 256, hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess) return false;
+    void* dp = nullptr;
+    if (hipHostGetDevicePointer(&dp, p, 0) != hipSuccess) {
+      (void)hipHostFree(p);
+      return false;
+    }
+    h = static_cast<unsigned long long*>(p);
+    d = static_cast<unsigned long long*>(dp);
+    __atomic_store_n(h, 0ull, __ATOMIC_RELEASE);
+    return true;
+  }
+};
+thread_local PinnedStatus t_status;
+
+struct PassStatus {
+  int steps, maxlag;
+};
+
+// Waits until the scheduler kernel of this pass (tag) has reported at least
+// `steps` steps.  The stream is polled now and then: if it has drained or
+// failed without the word, or a minute passes, the wait ends with an error.
+int wait_status(hipStream_t s, uint32_t tag, int steps, PassStatus* out) {
+  const auto t0 = std::chrono::steady_clock::now();
+  for (long iter = 0;; ++iter) {
+    const unsigned long long v = __atomic_load_n(t_status.h, __ATOMIC_ACQUIRE);
+    if ((uint32_t)(v >> 48) == (tag & 0xffffu) && (int)((v >> 16) & 0xffffffffull) >= steps) {
+      out->steps = (int)((v >> 16) & 0xffffffffull);
+      out->maxlag = (int)(v & 0xffffull);
+      return EB_OK;
+    }
+    if ((iter & 1023) == 1023) {
+      const hipError_t q = hipStreamQuery(s);
+      if (q == hipSuccess) {
+        const unsigned long long w = __atomic_load_n(t_status.h, __ATOMIC_ACQUIRE);
+        if ((uint32_t)(w >> 48) == (tag & 0xffffu) && (int)((w >> 16) & 0xffffffffull) >= steps) continue;
+        return set_error(EB_ERR_HIP, "device-scheduled pass: the stream drained before step %d reported", steps);
+      }
+      if (q != hipErrorNotReady)
+        return set_error(EB_ERR_HIP, "device-scheduled pass: %s", hipGetErrorString(q));
+      if (std::chrono::steady_clock::now() - t0 > std::chrono::seconds(60))
+        return set_error(EB_ERR_HIP, "device-scheduled pass: no report of step %d within 60 s", steps);
+    }
+    __builtin_ia32_pause();
+  }
+}
+
+// Algorithm 1 with the Schedule step on the GPU (see the file comment).
+// Inputs as validated by easybalance_run_pass; the layer-0 routing is queued.
+int run_pass_device(const eb_model_desc& d, int N, int T, const PassLayout& P, uint8_t* base, float* x,
+                    const float* gain, const void* const* Wg, const float* bias,
+                    const void* const* W_gu, const void* const* W_dn, int policy, int m,
+                    int max_steps, int32_t* n_steps_out, uint64_t* runsets_out, int32_t* layers_out,
+                    int64_t* step_load_out, int32_t* groups_out, int32_t* layer_loads_out,
+                    hipStream_t s) {
+  const size_t eb = d.dtype == EB_DTYPE_BF16 ? 2 : 4;
+  DevPassArgs A;
+  memset(&A, 0, sizeof(A));
+  A.N = N;
+  A.T = T;
+  A.L = d.L;
+  A.H = d.H;
+  A.E = d.E;
+  A.k = d.k;
+  A.S = d.S;
+  A.D = d.D;
+  A.m = m;
+  A.policy = policy;
+  A.max_records = N * d.L;
+  if ((++t_status.tag & 0xffffu) == 0) ++t_status.tag;  // tag 0 is the word's initial value
+  A.tag = (int32_t)(t_status.tag & 0xffffu);
+  A.a = base + P.a;
+  A.a_stride = eb * (size_t)T * d.H;
+  A.z = reinterpret_cast<float*>(base + P.logits);
+  A.idx = reinterpret_cast<int32_t*>(base + P.idx);
+  A.w = reinterpret_cast<float*>(base + P.w);
+  A.x = x;
+  A.counts = reinterpret_cast<int32_t*>(base + P.counts);
+  A.gain = gain;
+  A.bias = bias;
+  for (int l = 0; l < d.L; ++l) A.Wg[l] = Wg[l];
+  A.state = reinterpret_cast<DevPassState*>(base + P.dstate);
+  A.rt = reinterpret_cast<RunTable*>(base + P.drt);
+  A.rb = reinterpret_cast<RouteBatch*>(base + P.drb);
+  A.rec_mask = reinterpret_cast<uint64_t*>(base + P.rec_mask);
+  A.rec_layers = reinterpret_cast<int32_t*>(base + P.rec_layers);
+  A.rec_load = reinterpret_cast<int64_t*>(base + P.rec_load);
+  A.rec_groups = reinterpret_cast<int32_t*>(base + P.rec_groups);
+  A.rec_layer_loads = reinterpret_cast<int32_t*>(base + P.rec_ll);
+  A.status = t_status.d;
+  WeightTable wt;
+  memset(&wt, 0, sizeof(wt));
+  for (int l = 0; l < d.L; ++l) {
+    wt.gu[l] = W_gu[l];
+    wt.dn[l] = W_dn[l];
+  }
+  void* o = base + P.o;
+  int32_t* inv = reinterpret_cast<int32_t*>(base + P.inv);
+  void* ws = base + P.ws;
+  if (launch_pass_init(A, s) != hipSuccess) return set_error(EB_ERR_HIP, "pass init launch");
+
+  int rc;
+  auto enqueue_step = [&]() -> int {
+    if (launch_sched_step(A, s) != hipSuccess) return set_error(EB_ERR_HIP, "scheduler launch");
+    if ((rc = enqueue_step_dev(d, N, T, A.rt, wt, ws, o, inv, s))) return rc;
+    for (int b = 0; b * kRouteBatch < N; ++b)
+      if (launch_route_batch_dev(d, A.rb + b, std::min(kRouteBatch, N - b * kRouteBatch), T, s) != hipSuccess)
+        return set_error(EB_ERR_HIP, "route launch");
+    return EB_OK;
+  };
+  // every micro-batch needs L steps; queue what is known to run, then wait
+  // for a report one step behind the last queued one
+  int queued = 0, bound = d.L;
+  PassStatus st{0, 0};
+  for (;;) {
+    for (; queued < bound; ++queued)
+      if ((rc = enqueue_step())) return rc;
+    if ((rc = wait_status(s, A.tag, queued >= 2 ? queued - 1 : queued, &st))) return rc;
+    if (st.maxlag == 0) break;  // st.steps == queued: the pass is complete
+    if (st.steps + st.maxlag == queued) {
+      if ((rc = wait_status(s, A.tag, queued, &st))) return rc;
+      if (st.maxlag == 0) break;
+    }
+    if (st.steps + st.maxlag <= queued)
+      return set_error(EB_ERR_HIP, "device-scheduled pass: report (%d steps, %d to go) below %d queued", st.steps,
+                       st.maxlag, queued);
+    bound = st.steps + st.maxlag;
+  }
+  const int n_steps = queued;
+  if (n_steps_out) *n_steps_out = n_steps;
+  const int rec = std::min(n_steps, max_steps);
+  auto fetch = [&](void* dst, const void* src, size_t bytes) -> int {
+    if (bytes == 0) return EB_OK;
+    if (hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToHost, s) != hipSuccess)
+      return set_error(EB_ERR_HIP, "record copy");
+    return EB_OK;
+  };
+  if (runsets_out && (rc = fetch(runsets_out, A.rec_mask, sizeof(uint64_t) * rec))) return rc;
+  if (layers_out && (rc = fetch(layers_out, A.rec_layers, sizeof(int32_t) * (size_t)rec * N))) return rc;
+  if (step_load_out && (rc = fetch(step_load_out, A.rec_load, sizeof(int64_t) * (size_t)rec * d.D))) return rc;
+  if (groups_out && (rc = fetch(groups_out, A.rec_groups, sizeof(int32_t) * rec))) return rc;
+  if (layer_loads_out &&
+      (rc = fetch(layer_loads_out, A.rec_layer_loads, sizeof(int32_t) * (size_t)N * d.L * d.D)))
+    return rc;
+  if ((runsets_out || layers_out || step_load_out || groups_out || layer_loads_out) &&
+      hipStreamSynchronize(s) != hipSuccess)
+    return set_error(EB_ERR_HIP, "record copy: %s", hipGetErrorString(hipGetLastError()));
+  return EB_OK;
+}
 
 }  // namespace
 }  // namespace eb
@@ -107,12 +288,19 @@ int easybalance_run_pass(const eb_model_desc* desc, int32_t N, int32_t T, float*
   if (x == nullptr || gain == nullptr || Wg == nullptr || bias == nullptr || W_gu == nullptr ||
       W_dn == nullptr)
     return set_error(EB_ERR_INVALID_ARG, "a required pass pointer is NULL");
+  const bool device = (policy & EB_PASS_DEVICE_SCHEDULE) != 0;
+  policy &= ~EB_PASS_DEVICE_SCHEDULE;
   if (policy < EB_POLICY_MAXUTIL || policy > EB_POLICY_LOCKSTEP)
     return set_error(EB_ERR_INVALID_ARG, "policy %d unknown", policy);
   if (policy == EB_POLICY_MAXUTIL && N > EB_MAXUTIL_MAX_POOL)
     return set_error(EB_ERR_UNSUPPORTED, "MaxUtil enumerates subsets of at most %d micro-batches",
                      EB_MAXUTIL_MAX_POOL);
   if (m < 1) return set_error(EB_ERR_INVALID_ARG, "m=%d < 1", m);
+  if (device && d.D > kDevMaxD)
+    return set_error(EB_ERR_UNSUPPORTED, "device-scheduled pass: D=%d > %d", d.D, kDevMaxD);
+  if (device && !route_batch_device_ok(d))
+    return set_error(EB_ERR_UNSUPPORTED, "device-scheduled pass: fp32 routing with E=%d needs a launch per entry",
+                     d.E);
   if (state == nullptr || (reinterpret_cast<uintptr_t>(state) % kAlignP) != 0)
     return set_error(EB_ERR_INVALID_ARG, "state must be non-NULL and 256-byte aligned");
   if (state_bytes < need)
@@ -164,8 +352,12 @@ int easybalance_run_pass(const eb_model_desc* desc, int32_t N, int32_t T, float*
     }
     return EB_OK;
   };
+  if (device && !t_status.ready()) return set_error(EB_ERR_HIP, "pinned status allocation failed");
   for (int j = 0; j < N; ++j) pool[j] = j;
   if ((rc = route(pool))) return rc;
+  if (device)
+    return run_pass_device(d, N, T, P, base, x, gain, Wg, bias, W_gu, W_dn, policy, m, max_steps, n_steps_out,
+                           runsets_out, layers_out, step_load_out, groups_out, layer_loads_out, s);
   std::vector<int32_t> pool_counts;
   std::vector<int64_t> load(d.D);
   std::vector<eb_work> run;

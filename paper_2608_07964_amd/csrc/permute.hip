@@ -30,9 +30,12 @@ constexpr int kScanThreads = 1024;
 
 __device__ __forceinline__ int clamp_expert(int e, int E) { return e < 0 ? 0 : (e >= E ? E - 1 : e); }
 
-__global__ __launch_bounds__(kPermChunk) void perm_count_kernel(RunTable rt, int32_t* __restrict__ hist) {
+template <class RTA>
+__global__ __launch_bounds__(kPermChunk) void perm_count_kernel(RTA rta, int32_t* __restrict__ hist) {
+  const RunTable& rt = rta.get();
   __shared__ int cnt[1024];
   const int b = blockIdx.x;
+  if (b >= rt.chunk_base[rt.n]) return;  // past the live chunks (grid sized for the largest step)
   for (int e = threadIdx.x; e < rt.E; e += blockDim.x) cnt[e] = 0;
   __syncthreads();
   const int rho = find_entry(rt.chunk_base, rt.n, b);
@@ -83,8 +86,9 @@ __device__ int block_exclusive_scan(int v, int* wtot, int* total) {
 // The histogram cells (chunk b, column c) go through LDS in windows of
 // kHistWindow / (E+S) chunks (one window unless the step is very large);
 // every global load of a phase is independent of the others.
+template <class RTA>
 __global__ __launch_bounds__(kScanThreads) void perm_scan_kernel(
-    RunTable rt, int n_chunks, const int32_t* __restrict__ hist, int32_t* __restrict__ chunk_base,
+    RTA rta, const int32_t* __restrict__ hist, int32_t* __restrict__ chunk_base,
     int32_t* __restrict__ offsets, int4* __restrict__ tiles, int32_t* __restrict__ n_tiles,
     int4* __restrict__ groups, int32_t* __restrict__ n_groups, int bm, int max_tiles,
     int32_t* __restrict__ work_ctr) {
@@ -92,9 +96,11 @@ __global__ __launch_bounds__(kScanThreads) void perm_scan_kernel(
   __shared__ int hl[kHistWindow];                // one window of histogram cells
   __shared__ int wtot[kScanWaves];
   __shared__ int s_cb[EB_MAX_RUN + 1], s_tb[EB_MAX_RUN + 1], s_ly[EB_MAX_RUN];
+  const RunTable& rt = rta.get();
   const int tid = threadIdx.x;
   if (tid < kWorkCounters) work_ctr[tid] = 0;
   const int E = rt.E, ES = rt.E + rt.S, n = rt.n;
+  const int n_chunks = rt.chunk_base[n];
   const int n_keys = rt.L * ES;
   for (int i = tid; i < n_keys; i += kScanThreads) running[i] = 0;
   if (tid <= n) {
@@ -200,12 +206,15 @@ __global__ __launch_bounds__(kScanThreads) void perm_scan_kernel(
 }
 
 // One block per chunk, one token per thread.  `elem_bytes` is 2 (bf16) or 4.
+template <class RTA>
 __global__ __launch_bounds__(kPermChunk) void perm_scatter_kernel(
-    RunTable rt, const int32_t* __restrict__ chunk_base, int32_t* __restrict__ perm,
+    RTA rta, const int32_t* __restrict__ chunk_base, int32_t* __restrict__ perm,
     int32_t* __restrict__ inv) {
   __shared__ unsigned long long mask[kPermChunk / kWave][1024];
+  const RunTable& rt = rta.get();
   const int E = rt.E, S = rt.S, k = rt.k, ES = E + S, slots = k + S;
   const int b = blockIdx.x;
+  if (b >= rt.chunk_base[rt.n]) return;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   for (int i = threadIdx.x; i < (kPermChunk / kWave) * E; i += blockDim.x)
     mask[i / E][i % E] = 0ull;
@@ -241,13 +250,16 @@ __global__ __launch_bounds__(kPermChunk) void perm_scatter_kernel(
 
 // One wavefront per grouped row: a_perm[p] = a of perm[p].  A token's row is
 // read once per pair; used when a token has few pairs or short rows.
-__global__ __launch_bounds__(256) void gather_rows_kernel(RunTable rt, int P, int elem_bytes,
+template <class RTA>
+__global__ __launch_bounds__(256) void gather_rows_kernel(RTA rta, int elem_bytes,
                                                           const int32_t* __restrict__ perm,
                                                           uint8_t* __restrict__ a_perm) {
+  const RunTable& rt = rta.get();
   const int lane = threadIdx.x & 63;
   const int p = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (p >= P) return;
   const int slots = rt.k + rt.S;
+  const int P = rt.tok_base[rt.n] * slots;
+  if (p >= P) return;
   const int g = min(max(perm[p], 0), P - 1) / slots;  // global token of the pair
   const int rho = find_entry(rt.tok_base, rt.n, g);
   const int t = g - rt.tok_base[rho];
@@ -264,10 +276,12 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(RunTable rt, int P, in
 constexpr int kGatherU = 2;                  // 16-byte loads per lane per piece
 constexpr int kGatherPiece = 64 * kGatherU;  // 16-byte chunks per piece
 
-__global__ __launch_bounds__(256) void gather_tokens_kernel(RunTable rt, int total, int pieces,
-                                                          int elem_bytes,
+template <class RTA>
+__global__ __launch_bounds__(256) void gather_tokens_kernel(RTA rta, int pieces, int elem_bytes,
                                                           const int32_t* __restrict__ inv,
                                                           uint8_t* __restrict__ a_perm) {
+  const RunTable& rt = rta.get();
+  const int total = rt.tok_base[rt.n];
   const int lane = threadIdx.x & 63;
   const long long wv = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (wv >= (long long)total * pieces) return;
@@ -300,52 +314,99 @@ __global__ __launch_bounds__(256) void gather_tokens_kernel(RunTable rt, int tot
 
 }  // namespace
 
-hipError_t launch_perm_count(const RunTable& rt, int n_chunks, int32_t* hist, hipStream_t s) {
+// Launch helpers shared by the host-built (ByValue) and device-written
+// (InMemory) tables; grids are the live sizes or the largest step's.
+namespace {
+
+template <class RTA>
+void perm_count_impl(RTA a, int grid, int32_t* hist, hipStream_t s) {
   prof_start(EB_K_PERM_COUNT, s);
-  hipLaunchKernelGGL(perm_count_kernel, dim3(n_chunks), dim3(kPermChunk), 0, s, rt, hist);
+  if (grid > 0) hipLaunchKernelGGL(perm_count_kernel<RTA>, dim3(grid), dim3(kPermChunk), 0, s, a, hist);
   prof_stop(EB_K_PERM_COUNT, s);
-  return hipGetLastError();
 }
 
-hipError_t launch_perm_scan(const RunTable& rt, int n_chunks, const int32_t* hist,
-                            int32_t* chunk_base, int32_t* offsets, int4* tiles,
-                            int32_t* n_tiles, int4* groups, int32_t* n_groups, int bm,
-                            int max_tiles, int32_t* work_ctr, hipStream_t s) {
-  if ((long)rt.L * (rt.E + rt.S) > kMaxKeys || rt.E + rt.S > kScanThreads || rt.n > EB_MAX_RUN)
-    return hipErrorInvalidValue;
+template <class RTA>
+void perm_scan_impl(RTA a, const int32_t* hist, int32_t* chunk_base, int32_t* offsets, int4* tiles,
+                    int32_t* n_tiles, int4* groups, int32_t* n_groups, int bm, int max_tiles,
+                    int32_t* work_ctr, hipStream_t s) {
   prof_start(EB_K_PERM_SCAN, s);
-  hipLaunchKernelGGL(perm_scan_kernel, dim3(1), dim3(kScanThreads), 0, s, rt, n_chunks, hist,
-                     chunk_base, offsets, tiles, n_tiles, groups, n_groups, bm, max_tiles,
-                     work_ctr);
+  hipLaunchKernelGGL(perm_scan_kernel<RTA>, dim3(1), dim3(kScanThreads), 0, s, a, hist, chunk_base,
+                     offsets, tiles, n_tiles, groups, n_groups, bm, max_tiles, work_ctr);
   prof_stop(EB_K_PERM_SCAN, s);
-  return hipGetLastError();
 }
 
-hipError_t launch_perm_scatter(const RunTable& rt, int n_chunks, int P, int elem_bytes,
-                               const int32_t* chunk_base, int32_t* perm, int32_t* inv,
-                               void* a_perm, hipStream_t s) {
+// read each token's row once when that saves >= 32 KB of re-reads per
+// token (many pairs of long rows: the DeepSeek-V3 shape); else one
+// wavefront per grouped row, which keeps more wavefronts in flight
+bool gather_by_token(int slots, size_t row_bytes) { return (size_t)(slots - 1) * row_bytes >= 32768; }
+
+// grid_chunks / grid_tokens: chunks and tokens the grids cover
+template <class RTA>
+void perm_scatter_impl(RTA a, int slots, int H, int grid_chunks, int grid_tokens, int elem_bytes,
+                       const int32_t* chunk_base, int32_t* perm, int32_t* inv, void* a_perm,
+                       hipStream_t s) {
   prof_start(EB_K_PERM_SCATTER, s);
-  hipLaunchKernelGGL(perm_scatter_kernel, dim3(n_chunks), dim3(kPermChunk), 0, s, rt, chunk_base,
-                     perm, inv);
+  if (grid_chunks > 0)
+    hipLaunchKernelGGL(perm_scatter_kernel<RTA>, dim3(grid_chunks), dim3(kPermChunk), 0, s, a,
+                       chunk_base, perm, inv);
   prof_stop(EB_K_PERM_SCATTER, s);
-  // read each token's row once when that saves >= 32 KB of re-reads per
-  // token (many pairs of long rows: the DeepSeek-V3 shape); else one
-  // wavefront per grouped row, which keeps more wavefronts in flight
-  const int slots = rt.k + rt.S;
-  const size_t row_bytes = (size_t)rt.H * elem_bytes;
+  const size_t row_bytes = (size_t)H * elem_bytes;
   prof_start(EB_K_PERM_GATHER, s);
-  if ((size_t)(slots - 1) * row_bytes >= 32768) {
-    const int total = P / slots;
-    const int n16 = (int)(row_bytes / 16);
-    const int pieces = (n16 + kGatherPiece - 1) / kGatherPiece;
-    const long long waves = (long long)total * pieces;
-    hipLaunchKernelGGL(gather_tokens_kernel, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s, rt,
-                       total, pieces, elem_bytes, inv, static_cast<uint8_t*>(a_perm));
-  } else {
-    hipLaunchKernelGGL(gather_rows_kernel, dim3((P + 3) / 4), dim3(256), 0, s, rt, P, elem_bytes, perm,
-                       static_cast<uint8_t*>(a_perm));
+  if (grid_tokens > 0) {
+    if (gather_by_token(slots, row_bytes)) {
+      const int n16 = (int)(row_bytes / 16);
+      const int pieces = (n16 + kGatherPiece - 1) / kGatherPiece;
+      const long long waves = (long long)grid_tokens * pieces;
+      hipLaunchKernelGGL(gather_tokens_kernel<RTA>, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s,
+                         a, pieces, elem_bytes, inv, static_cast<uint8_t*>(a_perm));
+    } else {
+      const long long P = (long long)grid_tokens * slots;
+      hipLaunchKernelGGL(gather_rows_kernel<RTA>, dim3((unsigned)((P + 3) / 4)), dim3(256), 0, s, a,
+                         elem_bytes, perm, static_cast<uint8_t*>(a_perm));
+    }
   }
   prof_stop(EB_K_PERM_GATHER, s);
+}
+
+bool scan_fits(int L, int E, int S, int n) {
+  return (long)L * (E + S) <= kMaxKeys && E + S <= kScanThreads && n <= EB_MAX_RUN;
+}
+
+}  // namespace
+
+hipError_t launch_perm_count(const RunTable& rt, int n_chunks, int32_t* hist, hipStream_t s) {
+  perm_count_impl(ByValue<RunTable>{rt}, n_chunks, hist, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_perm_scan(const RunTable& rt, const int32_t* hist, int32_t* chunk_base,
+                            int32_t* offsets, int4* tiles, int32_t* n_tiles, int4* groups,
+                            int32_t* n_groups, int bm, int max_tiles, int32_t* work_ctr,
+                            hipStream_t s) {
+  if (!scan_fits(rt.L, rt.E, rt.S, rt.n)) return hipErrorInvalidValue;
+  perm_scan_impl(ByValue<RunTable>{rt}, hist, chunk_base, offsets, tiles, n_tiles, groups, n_groups,
+                 bm, max_tiles, work_ctr, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_perm_scatter(const RunTable& rt, int n_chunks, int elem_bytes,
+                               const int32_t* chunk_base, int32_t* perm, int32_t* inv,
+                               void* a_perm, hipStream_t s) {
+  perm_scatter_impl(ByValue<RunTable>{rt}, rt.k + rt.S, rt.H, n_chunks, rt.tok_base[rt.n], elem_bytes,
+                    chunk_base, perm, inv, a_perm, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_permute_dev(const eb_model_desc& d, const RunTable* rt, int max_chunks,
+                              int max_tokens, const StepBuffers& b, hipStream_t s) {
+  if (!scan_fits(d.L, d.E, d.S, 0)) return hipErrorInvalidValue;
+  const InMemory<RunTable> a{rt};
+  const int eb = d.dtype == EB_DTYPE_BF16 ? 2 : 4;
+  perm_count_impl(a, max_chunks, b.hist, s);
+  perm_scan_impl(a, b.hist, b.chunk_base, b.offsets, b.tiles, b.n_tiles, b.groups, b.n_groups,
+                 gemm_bm(d.dtype), b.max_tiles, b.work_ctr, s);
+  perm_scatter_impl(a, d.k + d.S, d.H, max_chunks, max_tokens, eb, b.chunk_base, b.perm, b.inv,
+                    b.a_perm, s);
   return hipGetLastError();
 }
 

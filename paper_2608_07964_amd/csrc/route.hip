@@ -67,8 +67,9 @@ __device__ __forceinline__ float4 normed(float4 v, float r, float4 g) {
 
 // ---------------------------------------------------------------------------
 // RMSNorm + cast, one wavefront per token.
-template <typename TA>
-__global__ __launch_bounds__(256) void rmsnorm_kernel(RouteBatch rb, int H, float eps) {
+template <typename TA, class RBA>
+__global__ __launch_bounds__(256) void rmsnorm_kernel(RBA rba, int H, float eps) {
+  const RouteBatch& rb = rba.get();
   const int lane = threadIdx.x & 63;
   const int g = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (g >= rb.tok0[rb.n]) return;
@@ -239,8 +240,11 @@ __device__ __forceinline__ void topk_group8(int sub, int E, int k, int norm_topk
 // Expert counts of a micro-batch from its picks, one workgroup per batch entry
 // (an LDS histogram, then one plain store per expert: nothing to clear
 // beforehand; an entry without tokens gets zeros).
-__global__ __launch_bounds__(1024) void counts_kernel(RouteBatch rb, int k, int E) {
+template <class RBA>
+__global__ __launch_bounds__(1024) void counts_kernel(RBA rba, int k, int E) {
+  const RouteBatch& rb = rba.get();
   const int ei = blockIdx.x;
+  if (ei >= rb.n) return;  // past the live entries (grid sized for a full batch)
   const int n = (rb.tok0[ei + 1] - rb.tok0[ei]) * k;
   const int32_t* __restrict__ idx = rb.e[ei].idx;
   int32_t* __restrict__ counts = rb.e[ei].counts;
@@ -355,11 +359,13 @@ template <> struct Vec8<float> {
 constexpr int kTokChunks = 4;  // 8-element chunks per thread: H <= 256 * 8 * 4
 constexpr int kTokMaxH = 256 * 8 * kTokChunks;
 
-template <typename TA, int EMAX>
-__global__ __launch_bounds__(256) void route_token_kernel(RouteBatch rb, int H, int E, int k,
+template <typename TA, int EMAX, class RBA>
+__global__ __launch_bounds__(256) void route_token_kernel(RBA rba, int H, int E, int k,
                                                           int norm_topk, float eps) {
   __shared__ float red[4];
   __shared__ float red_z[4][EMAX + 1];
+  const RouteBatch& rb = rba.get();
+  if ((int)blockIdx.x >= rb.tok0[rb.n]) return;  // past the live tokens
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int ei = find_entry(rb.tok0, rb.n, blockIdx.x);
   const int t = blockIdx.x - rb.tok0[ei];
@@ -450,12 +456,14 @@ __global__ __launch_bounds__(256) void route_token_kernel(RouteBatch rb, int H, 
 // partials in LDS and wave 0 adds them in that order, then the bias (a fixed
 // summation order), and writes the logits to z and to an LDS tile from which
 // 8 lanes per token pick its top-k.
-template <int NB>
-__global__ __launch_bounds__(256) void route_mfma_kernel(RouteBatch rb, int H, int E, int k,
+template <int NB, class RBA>
+__global__ __launch_bounds__(256) void route_mfma_kernel(RBA rba, int H, int E, int k,
                                                          int norm_topk) {
   constexpr int ZS = NB * 32 + 1;  // padded LDS row of the logit tile
   __shared__ float part[3][NB][16][64];
   __shared__ float zs[32][ZS];
+  const RouteBatch& rb = rba.get();
+  if ((int)blockIdx.x >= rb.blk0[rb.n]) return;  // past the live 32-token blocks
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lrow = lane & 31, khalf = lane >> 5;
   const int ei = find_entry(rb.blk0, rb.n, blockIdx.x);
@@ -564,37 +572,49 @@ __global__ __launch_bounds__(256) void topk_kernel(int T, int E, int k, int norm
   topk_token(E, k, norm_topk, [&](int e) { return zr[e]; }, idx + (size_t)t * k, w + (size_t)t * k);
 }
 
+// Whether the routing of a batch runs in a fixed set of launches (no launch
+// per entry): every bf16 stack, and fp32 stacks on the fused per-token path.
 template <typename TA>
-hipError_t route_batch_typed(const eb_model_desc& d, const RouteBatch& rb, hipStream_t s) {
-  const int total = rb.tok0[rb.n];
-  if (total > 0) {
-    const bool fused_token = (sizeof(TA) == 2 ? d.E <= 8 : d.E <= 64) && d.H <= kTokMaxH;
-    if (fused_token) {
+bool fused_token_path(const eb_model_desc& d) {
+  return (sizeof(TA) == 2 ? d.E <= 8 : d.E <= 64) && d.H <= kTokMaxH;
+}
+
+// grid_entries / grid_tokens / grid_blocks: entries, tokens and 32-token
+// blocks the grids cover (the live batch's, or a full batch's when the table
+// is in device memory); host_rb: the table itself when the host built it
+// (the fp32 per-entry path needs it).
+template <typename TA, class RBA>
+hipError_t route_batch_typed(const eb_model_desc& d, RBA rba, const RouteBatch* host_rb, int grid_entries,
+                             int grid_tokens, int grid_blocks, hipStream_t s) {
+  if (grid_tokens > 0) {
+    if (fused_token_path<TA>(d)) {
       prof_start(EB_K_ROUTE_LOGITS, s);
       if (d.E <= 8)
-        hipLaunchKernelGGL((route_token_kernel<TA, 8>), dim3(total), dim3(256), 0, s, rb, d.H, d.E,
-                           d.k, d.norm_topk, d.rms_eps);
+        hipLaunchKernelGGL((route_token_kernel<TA, 8, RBA>), dim3(grid_tokens), dim3(256), 0, s, rba, d.H,
+                           d.E, d.k, d.norm_topk, d.rms_eps);
       else
-        hipLaunchKernelGGL((route_token_kernel<TA, 64>), dim3(total), dim3(256), 0, s, rb, d.H,
+        hipLaunchKernelGGL((route_token_kernel<TA, 64, RBA>), dim3(grid_tokens), dim3(256), 0, s, rba, d.H,
                            d.E, d.k, d.norm_topk, d.rms_eps);
       prof_stop(EB_K_ROUTE_LOGITS, s);
     } else {
       prof_start(EB_K_ROUTE_NORM, s);
-      hipLaunchKernelGGL(rmsnorm_kernel<TA>, dim3((total + 3) / 4), dim3(256), 0, s, rb, d.H,
+      hipLaunchKernelGGL((rmsnorm_kernel<TA, RBA>), dim3((grid_tokens + 3) / 4), dim3(256), 0, s, rba, d.H,
                          d.rms_eps);
       prof_stop(EB_K_ROUTE_NORM, s);
       prof_start(EB_K_ROUTE_LOGITS, s);
       if (sizeof(TA) == 2) {
-        const dim3 grid(rb.blk0[rb.n]);
+        const dim3 grid(grid_blocks);
         const int nb = (d.E + 31) / 32;
         if (nb <= 2)
-          hipLaunchKernelGGL(route_mfma_kernel<2>, grid, dim3(256), 0, s, rb, d.H, d.E, d.k, d.norm_topk);
+          hipLaunchKernelGGL((route_mfma_kernel<2, RBA>), grid, dim3(256), 0, s, rba, d.H, d.E, d.k, d.norm_topk);
         else if (nb <= 4)
-          hipLaunchKernelGGL(route_mfma_kernel<4>, grid, dim3(256), 0, s, rb, d.H, d.E, d.k, d.norm_topk);
+          hipLaunchKernelGGL((route_mfma_kernel<4, RBA>), grid, dim3(256), 0, s, rba, d.H, d.E, d.k, d.norm_topk);
         else
-          hipLaunchKernelGGL(route_mfma_kernel<8>, grid, dim3(256), 0, s, rb, d.H, d.E, d.k, d.norm_topk);
+          hipLaunchKernelGGL((route_mfma_kernel<8, RBA>), grid, dim3(256), 0, s, rba, d.H, d.E, d.k, d.norm_topk);
         prof_stop(EB_K_ROUTE_LOGITS, s);
       } else {
+        if (host_rb == nullptr) return hipErrorInvalidValue;
+        const RouteBatch& rb = *host_rb;
         for (int i = 0; i < rb.n; ++i) {
           const int T = rb.tok0[i + 1] - rb.tok0[i];
           if (T == 0) continue;
@@ -617,7 +637,8 @@ hipError_t route_batch_typed(const eb_model_desc& d, const RouteBatch& rb, hipSt
     }
   }
   prof_start(EB_K_ROUTE_TOPK, s);
-  hipLaunchKernelGGL(counts_kernel, dim3(rb.n), dim3(1024), 0, s, rb, d.k, d.E);
+  if (grid_entries > 0)
+    hipLaunchKernelGGL((counts_kernel<RBA>), dim3(grid_entries), dim3(1024), 0, s, rba, d.k, d.E);
   prof_stop(EB_K_ROUTE_TOPK, s);
   return hipGetLastError();
 }
@@ -625,8 +646,23 @@ hipError_t route_batch_typed(const eb_model_desc& d, const RouteBatch& rb, hipSt
 }  // namespace
 
 hipError_t launch_route_batch(const eb_model_desc& d, const RouteBatch& rb, hipStream_t s) {
-  if (d.dtype == EB_DTYPE_BF16) return route_batch_typed<bf16_t>(d, rb, s);
-  return route_batch_typed<float>(d, rb, s);
+  const ByValue<RouteBatch> a{rb};
+  if (d.dtype == EB_DTYPE_BF16)
+    return route_batch_typed<bf16_t>(d, a, &rb, rb.n, rb.tok0[rb.n], rb.blk0[rb.n], s);
+  return route_batch_typed<float>(d, a, &rb, rb.n, rb.tok0[rb.n], rb.blk0[rb.n], s);
+}
+
+bool route_batch_device_ok(const eb_model_desc& d) {
+  return d.dtype == EB_DTYPE_BF16 || fused_token_path<float>(d);
+}
+
+hipError_t launch_route_batch_dev(const eb_model_desc& d, const RouteBatch* rb, int max_entries, int T,
+                                  hipStream_t s) {
+  if (!route_batch_device_ok(d) || max_entries > kRouteBatch) return hipErrorInvalidValue;
+  const InMemory<RouteBatch> a{rb};
+  const int tokens = max_entries * T, blocks = max_entries * ((T + 31) / 32);
+  if (d.dtype == EB_DTYPE_BF16) return route_batch_typed<bf16_t>(d, a, nullptr, max_entries, tokens, blocks, s);
+  return route_batch_typed<float>(d, a, nullptr, max_entries, tokens, blocks, s);
 }
 
 hipError_t launch_route(const eb_model_desc& d, int T, const float* x, const float* gain,

@@ -115,13 +115,16 @@ class Stack:
 
     # ---- Algorithm 1, natively ----------------------------------------------
     def run_native(self, policy: str = "maxutil", m: int | None = None, record: bool = True,
-                   stream=None) -> list[StepRecord]:
+                   stream=None, device_schedule: bool = False) -> list[StepRecord]:
         """The same pass as run(), driven by easybalance_run_pass (the host
-        loop in the library).  Fills layer_loads and returns the steps when
+        loop in the library; device_schedule: Schedule on the GPU, the host
+        queueing steps ahead).  Fills layer_loads and returns the steps when
         record (records cover the first N*L steps, i.e. all of them)."""
         if stream is None:
             stream = torch.cuda.current_stream(self.dev)
         pol = B.EB_POLICY_LOCKSTEP if policy == "lockstep" else POLICIES[policy]
+        if device_schedule:
+            pol |= B.EB_PASS_DEVICE_SCHEDULE
         m = self.N if m is None else m
         if not hasattr(self, "_state"):
             self._state_bytes = B.easybalance_pass_state_size(self.desc, self.N, self.T)

@@ -170,6 +170,21 @@ def test_run_pass_rejects_bad_arguments_before_touching_the_gpu():
     with pytest.raises(B.EasyBalanceError) as e:   # m < 1
         B.easybalance_run_pass(*args, B.EB_POLICY_MAXUTIL, 0, fake, need)
     assert e.value.code == B.EB_ERR_INVALID_ARG
+    with pytest.raises(B.EasyBalanceError) as e:   # a flag bit other than EB_PASS_DEVICE_SCHEDULE
+        B.easybalance_run_pass(*args, B.EB_POLICY_MAXUTIL | 0x200, 3, fake, need)
+    assert e.value.code == B.EB_ERR_INVALID_ARG
+    wide = B.make_desc(2, 256, 128, 128, 2, 0, 128, "bf16")   # D = 128 virtual devices
+    need_w = B.easybalance_pass_state_size(wide, 4, 64)
+    args_w = (wide, 4, 64, fake, fake, [fake, fake], fake, [fake, fake], [fake, fake])
+    with pytest.raises(B.EasyBalanceError) as e:   # the device scheduler handles D <= 64
+        B.easybalance_run_pass(*args_w, B.EB_POLICY_MAXUTIL | B.EB_PASS_DEVICE_SCHEDULE, 3, fake, need_w)
+    assert e.value.code == B.EB_ERR_UNSUPPORTED
+    f32 = B.make_desc(2, 256, 128, 128, 2, 0, 4, "f32")        # fp32 routing with E > 64
+    need_f = B.easybalance_pass_state_size(f32, 4, 64)
+    args_f = (f32, 4, 64, fake, fake, [fake, fake], fake, [fake, fake], [fake, fake])
+    with pytest.raises(B.EasyBalanceError) as e:
+        B.easybalance_run_pass(*args_f, B.EB_POLICY_CUMUTIL | B.EB_PASS_DEVICE_SCHEDULE, 3, fake, need_f)
+    assert e.value.code == B.EB_ERR_UNSUPPORTED
 
 
 def test_pack_weights_rejects_bad_arguments_before_touching_the_gpu():

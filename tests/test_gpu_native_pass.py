@@ -1,7 +1,8 @@
-"""The native Algorithm-1 driver (easybalance_run_pass) against the Python
-driver over the same entry points: identical schedules, loads, group counts
-and bit-identical hidden states, for every policy, on the small stacks and on
-the full-size Mixtral-shaped stack that bench.py times."""
+"""The native Algorithm-1 driver (easybalance_run_pass), host- and
+device-scheduled, against the Python driver over the same entry points:
+identical schedules, loads, group counts and bit-identical hidden states, for
+every policy, on the small stacks and on the full-size Mixtral-shaped stack
+that bench.py times."""
 import numpy as np
 import pytest
 import torch
@@ -13,8 +14,12 @@ from gpu_helpers import log, make_stack
 
 pytestmark = pytest.mark.gpu
 
-SMALL = [c if c.dtype == "f32" else mini(c) for c in CONFIGS] + [mini(BY_NAME["mixtral_bf16"], H=256, F=8192, T=96, L=2)]
-SMALL_IDS = [c.name for c in SMALL[:-1]] + [SMALL[-1].name + "_longk"]
+# plus a split-K down GEMM (F >= 8192) and the read-once gather (k+S = 9
+# slots of 4 KB rows)
+SMALL = ([c if c.dtype == "f32" else mini(c) for c in CONFIGS]
+         + [mini(BY_NAME["mixtral_bf16"], H=256, F=8192, T=96, L=2),
+            mini(BY_NAME["dsv3_share_bf16"], H=2048, T=96, L=2)])
+SMALL_IDS = [c.name for c in SMALL[:-2]] + [SMALL[-2].name + "_longk", SMALL[-1].name + "_rowonce"]
 
 
 def _compare(cfg, device, policies):
@@ -24,15 +29,17 @@ def _compare(cfg, device, policies):
         py_steps = st.run(policy, m=m)
         torch.cuda.synchronize()
         x_py, ll_py = st.x.clone(), st.layer_loads.copy()
-        st.x.copy_(inp.x0)
-        nat_steps = st.run_native(policy, m=m)
-        torch.cuda.synchronize()
-        assert torch.equal(st.x, x_py), (policy, m)
-        assert np.array_equal(st.layer_loads, ll_py), (policy, m)
-        assert [s.runset for s in nat_steps] == [s.runset for s in py_steps], (policy, m)
-        for a, b in zip(nat_steps, py_steps):
-            assert np.array_equal(a.load, b.load) and a.groups == b.groups and a.pairs == b.pairs
-        log(f"  {cfg.name} {policy} m={m}: {len(nat_steps)} steps identical")
+        for dev_sched in (False, True):
+            st.x.copy_(inp.x0)
+            nat_steps = st.run_native(policy, m=m, device_schedule=dev_sched)
+            torch.cuda.synchronize()
+            what = (policy, m, "device" if dev_sched else "host")
+            assert torch.equal(st.x, x_py), what
+            assert np.array_equal(st.layer_loads, ll_py), what
+            assert [s.runset for s in nat_steps] == [s.runset for s in py_steps], what
+            for a, b in zip(nat_steps, py_steps):
+                assert np.array_equal(a.load, b.load) and a.groups == b.groups and a.pairs == b.pairs, what
+        log(f"  {cfg.name} {policy} m={m}: {len(nat_steps)} steps identical (host and device schedule)")
 
 
 @pytest.mark.parametrize("cfg", SMALL, ids=SMALL_IDS)
