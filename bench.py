@@ -111,7 +111,7 @@ def main() -> int:
     ap.add_argument("--config", default="mixtral_bf16")
     ap.add_argument("--policy", default="maxutil", choices=["maxutil", "cumutil", "diffpeak", "lockstep"])
     ap.add_argument("--m", type=int, default=None, help="minimum combination size (default 0.75 N)")
-    ap.add_argument("--schedule", default="host", choices=["host", "device"],
+    ap.add_argument("--schedule", default="device", choices=["host", "device"],
                     help="where Algorithm 1's Schedule runs: on the host after a copy of the pool's "
                          "expert counts each step, or in a kernel on the GPU with the host queueing "
                          "steps ahead")
