@@ -28,6 +28,10 @@ constexpr int kSchedThreads = 512;
 // products a.num * b.den and b.num * a.den, compared high word first.
 __device__ __forceinline__ int ratio_cmp(unsigned long long an, unsigned long long ad, unsigned long long bn,
                                          unsigned long long bd) {
+  if (((an | ad | bn | bd) >> 32) == 0) {  // the products fit in 64 bits
+    const unsigned long long l = an * bd, r = bn * ad;
+    return l > r ? 1 : (l < r ? -1 : 0);
+  }
   const unsigned long long lh = __umul64hi(an, bd), ll = an * bd;
   const unsigned long long rh = __umul64hi(bn, ad), rl = bn * ad;
   if (lh != rh) return lh > rh ? 1 : -1;
@@ -179,6 +183,7 @@ __global__ __launch_bounds__(kSchedThreads) void sched_step_kernel(DevPassArgs A
   for (int w = tid; w < kDevMaxKeyWords; w += kSchedThreads) s_bits[w] = 0u;
   for (int w = tid; w < kDevMaxNzWords; w += kSchedThreads) s_nz[w] = 0u;
   for (int i = tid; i < EB_MAX_POOL * kDevMaxD; i += kSchedThreads) s_load[i] = 0;
+  if (tid < kDevMaxD) s_tot[tid] = 0;
   if (tid < EB_MAX_LAYERS / 32) s_lbits[tid] = 0u;
   // the pool, in ascending id: one ballot over wave 0's lanes (N <= 64)
   const unsigned long long pool_mask = __ballot(tid < N && my_layer < L);
@@ -237,6 +242,7 @@ __global__ __launch_bounds__(kSchedThreads) void sched_step_kernel(DevPassArgs A
         const int pi = i / E, e = i - pi * E;
         atomicAdd(reinterpret_cast<unsigned long long*>(&s_load[pi * kDevMaxD + e / per]),
                   (unsigned long long)c[u]);
+        atomicAdd(reinterpret_cast<unsigned long long*>(&s_tot[e / per]), (unsigned long long)c[u]);
         atomicOr(&s_nz[i >> 5], 1u << (i & 31));
       }
     }
@@ -255,26 +261,29 @@ __global__ __launch_bounds__(kSchedThreads) void sched_step_kernel(DevPassArgs A
     // every subset with >= need members (n <= EB_MAXUTIL_MAX_POOL) as the
     // complement of an excluded set X, |X| <= n - need: sum_j C(n, j) of
     // them, numbered consecutively (by |X|, then X's rank) and cut into one
-    // contiguous range per thread; the pool's total workload minus X's
-    // members gives each one's.  The best of each thread, of each wavefront,
-    // then of the block.
-    for (int d = tid; d < D; d += kSchedThreads) {
-      long long v = 0;
-      for (int i = 0; i < n; ++i) v += s_load[i * kDevMaxD + d];
-      s_tot[d] = v;
-    }
-    __syncthreads();
+    // contiguous range per thread (one set per lane of wave 0 when there
+    // are at most 64); the pool's total workload (summed with the loads)
+    // minus X's members gives each one's.  The best of each thread, of each
+    // wavefront, then of the block.
     unsigned count = 0;
     for (int j = 0; j <= n - need; ++j) count += s_C[n * kMaxC + j];
-    const unsigned chunk = (count + kSchedThreads - 1) / kSchedThreads;
-    const unsigned r0 = min(count, (unsigned)tid * chunk), r1 = min(count, r0 + chunk);
-    Cand best = wave_best(maxutil_range<DMAX>(r0, r1, n, D, s_C, s_load, s_tot));
-    if (lane == 0) s_cand[wave] = best;
-    __syncthreads();
-    if (wave == 0) {
-      Cand c = lane < kSchedThreads / kWave ? s_cand[lane] : Cand{{0ull, 1ull}, -1, 0u};
-      c = wave_best(c);
-      if (lane == 0) s_chosen = c.set;
+    if (count <= (unsigned)kWave) {  // one candidate per lane of wave 0 at most
+      if (wave == 0) {
+        const unsigned r0 = lane, r1 = min(count, (unsigned)lane + 1u);
+        const Cand best = wave_best(maxutil_range<DMAX>(r0, r1, n, D, s_C, s_load, s_tot));
+        if (lane == 0) s_chosen = best.set;
+      }
+    } else {
+      const unsigned chunk = (count + kSchedThreads - 1) / kSchedThreads;
+      const unsigned r0 = min(count, (unsigned)tid * chunk), r1 = min(count, r0 + chunk);
+      Cand best = wave_best(maxutil_range<DMAX>(r0, r1, n, D, s_C, s_load, s_tot));
+      if (lane == 0) s_cand[wave] = best;
+      __syncthreads();
+      if (wave == 0) {
+        Cand c = lane < kSchedThreads / kWave ? s_cand[lane] : Cand{{0ull, 1ull}, -1, 0u};
+        c = wave_best(c);
+        if (lane == 0) s_chosen = c.set;
+      }
     }
   } else {
     if (A.policy == EB_POLICY_DIFFPEAK && tid < n) {  // peak device of each member: first maximum
