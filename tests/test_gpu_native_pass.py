@@ -51,3 +51,12 @@ def test_native_pass_matches_python_driver(cfg, device):
 def test_native_pass_full_size_bench_stack(device):
     cfg = [c for c in CONFIGS if c.name == "mixtral_bf16"][0]
     _compare(cfg, device, [("maxutil", cfg.m), ("lockstep", None)])
+
+
+def test_native_pass_pool_over_32_micro_batches(device):
+    """40 micro-batches: the routing after a step spans two batch tables
+    (32 entries each), host- and device-scheduled (MaxUtil enumerates pools
+    of at most 20, so the heuristics and lock-step run here)."""
+    cfg = mini(BY_NAME["qwen_moe_bf16"], N=40, T=24, L=2)
+    assert cfg.N == 40
+    _compare(cfg, device, [("cumutil", 30), ("diffpeak", 30), ("lockstep", None)])
