@@ -39,6 +39,11 @@ def _compare(cfg, device, policies):
             assert [s.runset for s in nat_steps] == [s.runset for s in py_steps], what
             for a, b in zip(nat_steps, py_steps):
                 assert np.array_equal(a.load, b.load) and a.groups == b.groups and a.pairs == b.pairs, what
+            # without records the call returns once the last step is queued
+            st.x.copy_(inp.x0)
+            assert st.run_native(policy, m=m, record=False, device_schedule=dev_sched) == []
+            torch.cuda.synchronize()
+            assert torch.equal(st.x, x_py), what + ("unrecorded",)
         log(f"  {cfg.name} {policy} m={m}: {len(nat_steps)} steps identical (host and device schedule)")
 
 
