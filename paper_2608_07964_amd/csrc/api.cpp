@@ -179,7 +179,7 @@ StepWs carve_step(const eb_model_desc& d, const StepShape& sh, const eb_step_vie
 // The two grouped GEMMs of a step whose permutation is queued before them.
 // sh.P rows are held by the buffers; the live rows come from the offsets.
 int run_gemms(const eb_model_desc& d, const StepShape& sh, const StepWs& w, const WeightTable& wt,
-              void* o, hipStream_t s) {
+              void* o, hipStream_t s, bool sum_halves = true) {
   GroupedProblem gp;
   gp.H = d.H;
   gp.F = d.F;
@@ -201,7 +201,7 @@ int run_gemms(const eb_model_desc& d, const StepShape& sh, const StepWs& w, cons
   gp.work_ctr = w.b.work_ctr + kWorkCounters / 2;
   gp.ksplit = down_ksplit(d.dtype, d.F);
   gp.partial = w.partial;
-  return hip_status(launch_down(d.dtype, gp, wt, w.h, o, s), "down GEMM");
+  return hip_status(launch_down(d.dtype, gp, wt, w.h, o, s, sum_halves), "down GEMM");
 }
 
 // ---- kernel timing ---------------------------------------------------------
@@ -242,7 +242,13 @@ int enqueue_step_dev(const eb_model_desc& d, int N, int T, const RunTable* rt, c
   int rc;
   if ((rc = hip_status(launch_permute_dev(d, rt, sh.n_chunks, (int)sh.tokens, w.b, s), "permute")))
     return rc;
-  if ((rc = run_gemms(d, sh, w, wt, o, s))) return rc;
+  // a split-K down GEMM leaves its two fp32 halves for the combine, which
+  // rounds their sum as the split-K sum kernel would (o is not stored)
+  const bool fuse = w.partial != nullptr;
+  if ((rc = run_gemms(d, sh, w, wt, o, s, !fuse))) return rc;
+  if (fuse)
+    return hip_status(launch_combine_split_dev(rt, (int)sh.tokens, w.partial, (long long)sh.P * d.H, inv, s),
+                      "combine");
   return hip_status(launch_combine_dev(rt, (int)sh.tokens, d.dtype, o, inv, s), "combine");
 }
 

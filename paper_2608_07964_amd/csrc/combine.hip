@@ -33,6 +33,17 @@ template <>
 struct Row8<bf16_t> {
   uint4 u;
   __device__ __forceinline__ void load(const bf16_t* p) { u = *reinterpret_cast<const uint4*>(p); }
+  // the row as a split-K down GEMM's sum would store it: bf16(p0 + p1),
+  // the halves `stride` floats apart
+  __device__ __forceinline__ void load_split(const float* p, long long stride) {
+    const float4 a0 = reinterpret_cast<const float4*>(p)[0], a1 = reinterpret_cast<const float4*>(p)[1];
+    const float4 b0 = reinterpret_cast<const float4*>(p + stride)[0];
+    const float4 b1 = reinterpret_cast<const float4*>(p + stride)[1];
+    u.x = (uint32_t)f32_to_bf16(a0.x + b0.x) | ((uint32_t)f32_to_bf16(a0.y + b0.y) << 16);
+    u.y = (uint32_t)f32_to_bf16(a0.z + b0.z) | ((uint32_t)f32_to_bf16(a0.w + b0.w) << 16);
+    u.z = (uint32_t)f32_to_bf16(a1.x + b1.x) | ((uint32_t)f32_to_bf16(a1.y + b1.y) << 16);
+    u.w = (uint32_t)f32_to_bf16(a1.z + b1.z) | ((uint32_t)f32_to_bf16(a1.w + b1.w) << 16);
+  }
   __device__ __forceinline__ float at(int i) const {
     const uint32_t w[4] = {u.x, u.y, u.z, u.w};
     const uint32_t x = w[i >> 1];
@@ -40,9 +51,14 @@ struct Row8<bf16_t> {
   }
 };
 
-template <typename TO, class RTA>
+// SPLIT (bf16 only): o is not stored; its rows are formed from the two fp32
+// K halves of the down GEMM at part and part + stride, rounded as the
+// split-K sum rounds them, so the result is the same bit for bit.
+template <typename TO, class RTA, bool SPLIT = false>
 __global__ __launch_bounds__(kCombThreads) void combine_kernel(RTA rta, const TO* __restrict__ o,
-                                                               const int32_t* __restrict__ inv) {
+                                                               const int32_t* __restrict__ inv,
+                                                               const float* __restrict__ part = nullptr,
+                                                               long long stride = 0) {
   __shared__ int s_row[kMaxSlots];
   __shared__ float s_w[kMaxSlots];
   const RunTable& rt = rta.get();
@@ -63,7 +79,12 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(RTA rta, const TO
     Row8<TO> v[kMaxSlots];
 #pragma unroll
     for (int r = 0; r < kMaxSlots; ++r)
-      if (r < slots) v[r].load(o + (size_t)s_row[r] * H + c);
+      if (r < slots) {
+        if constexpr (SPLIT)
+          v[r].load_split(part + (size_t)s_row[r] * H + c, stride);
+        else
+          v[r].load(o + (size_t)s_row[r] * H + c);
+      }
     float4 x0 = reinterpret_cast<float4*>(x + c)[0];
     float4 x1 = reinterpret_cast<float4*>(x + c)[1];
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
@@ -114,6 +135,16 @@ hipError_t launch_combine(const RunTable& rt, int dtype, const void* o, const in
 hipError_t launch_combine_dev(const RunTable* rt, int max_tokens, int dtype, const void* o,
                               const int32_t* inv, hipStream_t s) {
   combine_impl(InMemory<RunTable>{rt}, max_tokens, dtype, o, inv, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_combine_split_dev(const RunTable* rt, int max_tokens, const float* part, long long stride,
+                                    const int32_t* inv, hipStream_t s) {
+  prof_start(EB_K_COMBINE, s);
+  if (max_tokens > 0)
+    hipLaunchKernelGGL((combine_kernel<bf16_t, InMemory<RunTable>, true>), dim3(max_tokens), dim3(kCombThreads),
+                       0, s, InMemory<RunTable>{rt}, static_cast<const bf16_t*>(nullptr), inv, part, stride);
+  prof_stop(EB_K_COMBINE, s);
   return hipGetLastError();
 }
 

@@ -202,13 +202,19 @@ hipError_t launch_pack_weights(int dtype, int gateup, int n, int N, int K, int F
 
 hipError_t launch_gateup(int dtype, const GroupedProblem& p, const WeightTable& wt,
                          const void* a_perm, void* h, hipStream_t s);
+// sum_halves false (split K only): the fp32 halves stay in p.partial and o
+// is not written (launch_combine_split_dev reads them).
 hipError_t launch_down(int dtype, const GroupedProblem& p, const WeightTable& wt,
-                       const void* h, void* o, hipStream_t s);
+                       const void* h, void* o, hipStream_t s, bool sum_halves = true);
 
 hipError_t launch_combine(const RunTable& rt, int dtype, const void* o, const int32_t* inv,
                           hipStream_t s);
 hipError_t launch_combine_dev(const RunTable* rt, int max_tokens, int dtype, const void* o,
                               const int32_t* inv, hipStream_t s);
+// bf16 combine straight from a split-K down GEMM's fp32 halves (part and
+// part + stride), rounded as the split-K sum would round them.
+hipError_t launch_combine_split_dev(const RunTable* rt, int max_tokens, const float* part, long long stride,
+                                    const int32_t* inv, hipStream_t s);
 
 // Profiling hooks (api.cpp): bracket one launch of kernel class `kind`.
 void prof_start(int kind, hipStream_t s);

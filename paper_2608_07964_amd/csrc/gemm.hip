@@ -768,12 +768,12 @@ hipError_t launch_gateup(int dtype, const GroupedProblem& p, const WeightTable& 
 }
 
 hipError_t launch_down(int dtype, const GroupedProblem& p, const WeightTable& wt, const void* h,
-                       void* o, hipStream_t s) {
+                       void* o, hipStream_t s, bool sum_halves) {
   prof_start(EB_K_DOWN, s);
   if (dtype == EB_DTYPE_BF16) {
     hipLaunchKernelGGL(grouped_gemm_bf16<MODE_DOWN>, dim3(persistent_grid()), dim3(kThreads), 0, s,
                        p, wt, static_cast<const bf16_t*>(h), static_cast<bf16_t*>(o), p.H / BN);
-    if (p.ksplit > 1) {
+    if (p.ksplit > 1 && sum_halves) {
       const long long n = (long long)p.P * p.H;
       hipLaunchKernelGGL(split_sum_kernel, dim3((unsigned)((n / 4 + 255) / 256)), dim3(256), 0, s,
                          p.partial, n, p.P_live, p.H, static_cast<bf16_t*>(o));
