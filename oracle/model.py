@@ -78,6 +78,26 @@ def device_loads(counts: np.ndarray, D: int) -> np.ndarray:
     return counts.reshape(counts.shape[:-1] + (D, E // D)).sum(axis=-1)
 
 
+def placed_device_loads(counts: np.ndarray, copies, D: int) -> np.ndarray:
+    """Workload vector under a static placement with replicas (the redundant
+    experts of Section 5's orthogonality study with EPLB): copies[e] lists the
+    devices holding expert e in ascending order; an expert's c routed pairs
+    are split as evenly as possible over its r copies, the i-th copy taking
+    c // r pairs plus one if i < c % r.  Works on the last axis of counts."""
+    counts = np.asarray(counts, dtype=np.int64)
+    E = counts.shape[-1]
+    assert len(copies) == E
+    out = np.zeros(counts.shape[:-1] + (D,), dtype=np.int64)
+    for e in range(E):
+        devs = list(copies[e])
+        r = len(devs)
+        assert r >= 1 and devs == sorted(set(devs)) and all(0 <= d < D for d in devs)
+        c = counts[..., e]
+        for i, d in enumerate(devs):
+            out[..., d] += c // r + (c % r > i)
+    return out
+
+
 # --------------------------------------------------------------------------
 # experts and combine (Eq. 1 plus the residual add)
 # --------------------------------------------------------------------------

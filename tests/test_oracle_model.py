@@ -214,3 +214,93 @@ def test_run_plain_counts_and_loads():
     # layers run in order: x after layer l is the layer-l output of x before it
     out = model.moe_layer(run.x[1, 2], 1, P, E=E, k=k, S=S, eps=1e-6, dtype="bf16")
     assert np.array_equal(out.x_out, run.x[2, 2])
+
+
+def test_router_logits_bias_closed_form():
+    """One nonzero per router row: z[t, e] = c_e * a[t, p_e] + b_e, so a dropped,
+    negated, scaled or misindexed bias term (or a transposed router) changes z."""
+    rng = np.random.default_rng(11)
+    T, H, E = 6, 10, 7
+    Wg, pick, c = _selection(E, H, rng)
+    b = rng.normal(size=E) * 3.0
+    a = rng.normal(size=(T, H))
+    z = model.router_logits(a, Wg, b)
+    assert z.shape == (T, E)
+    for t in range(T):
+        for e in range(E):
+            assert z[t, e] == pytest.approx(c[e] * a[t, pick[e]] + b[e], rel=1e-15, abs=1e-15)
+    # a zero router leaves exactly the bias, in expert order, for every token
+    z0 = model.router_logits(a, np.zeros((E, H)), b)
+    assert np.array_equal(z0, np.broadcast_to(b, (T, E)))
+
+
+def test_routing_decided_by_the_bias_alone():
+    """Equal router rows give every expert the same a.Wg term, so the bias alone
+    orders the experts (Section 2.1: W, I = topk(G(h'))): the picks are the
+    experts of largest bias for every token, ties to the lower id, and the
+    weights are the softmax of the bias (a common shift cancels)."""
+    rng = np.random.default_rng(12)
+    T, H, E, k = 9, 16, 6, 3
+    row = rng.normal(size=H)
+    b = np.array([0.5, 2.0, -1.0, 2.0, 1.5, -3.0])      # experts 1 and 3 tie
+    P = model.Weights(gain=lambda l: np.ones(H), router=lambda l: np.tile(row, (E, 1)),
+                      bias=lambda l: b, gate_up=None, down=None)
+    x = rng.normal(size=(T, H))
+    a, z, idx, w, counts = model.route(x, 0, P, k=k, eps=1e-6, dtype="f32")
+    want = [1, 3, 4]                                    # 2.0 (id 1), 2.0 (id 3), 1.5
+    assert idx.tolist() == [want] * T
+    ez = [math.exp(v - 2.0) for v in b]
+    for t in range(T):
+        for r, e in enumerate(want):
+            assert w[t, r] == pytest.approx(ez[e] / sum(ez), rel=1e-12)
+    assert counts.tolist() == [0, T, 0, T, T, 0]
+    # with the bias dropped every expert ties and the picks would be 0, 1, 2
+    _, _, idx0, _, _ = model.route(x, 0, model.Weights(P.gain, P.router, lambda l: np.zeros(E),
+                                                       None, None), k=k, eps=1e-6, dtype="f32")
+    assert idx0.tolist() == [[0, 1, 2]] * T
+
+
+def test_topk_nan_logits_rank_last_and_stay_distinct():
+    """NaN logits sort after every number (stable argsort of -z), so a token
+    whose remaining logits are all NaN takes the lowest ids not yet picked and
+    its k picks are always distinct experts."""
+    z = np.array([[np.nan, 1.0, np.nan, -np.inf, np.nan],
+                  [np.nan] * 5,
+                  [-np.inf, -np.inf, np.nan, 0.0, np.nan]])
+    idx = model.topk_indices(z, 4)
+    assert idx.tolist() == [[1, 3, 0, 2], [0, 1, 2, 3], [3, 0, 1, 2]]
+    assert all(len(set(r)) == 4 for r in idx.tolist())
+
+
+def test_placed_device_loads_hand_worked():
+    """E = 3 on D = 2: expert 0 on both devices, 1 on device 0, 2 on device 1.
+    Counts (5, 2, 4): expert 0 splits 3 + 2 (the first copy takes the odd
+    pair), so device 0 carries 3 + 2 = 5 and device 1 carries 2 + 4 = 6."""
+    got = model.placed_device_loads(np.array([5, 2, 4]), [[0, 1], [0], [1]], 2)
+    assert got.tolist() == [5, 6]
+    # three copies of 7 pairs: 3, 2, 2
+    got = model.placed_device_loads(np.array([7, 0]), [[0, 2, 3], [1]], 4)
+    assert got.tolist() == [3, 0, 2, 2]
+
+
+def test_placed_device_loads_reduces_to_contiguous_blocks_and_brute_force():
+    rng = np.random.default_rng(13)
+    # one copy per expert at e // (E/D): the contiguous mapping exactly
+    for E, D in [(8, 4), (60, 4), (64, 8), (256, 32)]:
+        counts = rng.integers(0, 50, size=(3, 5, E))
+        contig = [[e // (E // D)] for e in range(E)]
+        assert np.array_equal(model.placed_device_loads(counts, contig, D), model.device_loads(counts, D))
+    # random placements: dealing each expert's pairs one at a time round-robin
+    # over its copies gives the same split; total work is conserved
+    for trial in range(200):
+        E, D = int(rng.integers(1, 9)), int(rng.integers(1, 6))
+        copies = [sorted(rng.choice(D, size=int(rng.integers(1, D + 1)), replace=False).tolist())
+                  for _ in range(E)]
+        counts = rng.integers(0, 20, size=E)
+        want = np.zeros(D, dtype=np.int64)
+        for e in range(E):
+            for p in range(int(counts[e])):
+                want[copies[e][p % len(copies[e])]] += 1
+        got = model.placed_device_loads(counts, copies, D)
+        assert np.array_equal(got, want), (copies, counts)
+        assert got.sum() == counts.sum()
