@@ -15,11 +15,17 @@
  *  - Return value: EB_OK (0) or a negative EB_ERR_* code.  On error the
  *    outputs are unspecified and easybalance_last_error() (thread-local)
  *    describes the first failed check.  No C++ exception crosses the ABI.
- *  - Memory: every buffer is owned by the caller.  "device" pointers are HIP
- *    device allocations on the current device; "host" pointers are ordinary
- *    host memory.  The library allocates no device memory; scratch space of
- *    easybalance_moe_step is a caller workspace sized by
- *    easybalance_moe_step_workspace_size.
+ *  - Memory: every buffer passed in is owned by the caller.  "device"
+ *    pointers are HIP device allocations on the current device; "host"
+ *    pointers are ordinary host memory.  The library allocates no device
+ *    memory; scratch space of easybalance_moe_step is a caller workspace
+ *    sized by easybalance_moe_step_workspace_size.  What the library does
+ *    hold, until the process (or the calling thread) ends:
+ *      easybalance_run_pass: per host thread, a pinned host buffer of the
+ *        pool's expert counts (host-scheduled passes, N * E int32, grown on
+ *        demand) and a 256-byte host-mapped status word (device-scheduled
+ *        passes); freed when the thread exits;
+ *      easybalance_profile_*: a process-wide pool of timing events.
  *  - Streams: `stream` is a hipStream_t passed as void* (NULL = null stream).
  *    Device calls only enqueue work on it and never synchronize; the caller
  *    orders calls on one stream or with events.
@@ -140,11 +146,15 @@ const char* easybalance_last_error(void);
  * Wg         device [E][H] dtype router weights
  * bias       device [E] fp32 router logit bias
  * a_out      device [T][H] dtype
- * logits_out device [T][E] fp32 (required: the router's output z)
+ * logits_out device [T][E] fp32: the router's output z, or NULL when it is
+ *            not wanted -- except on fp32 stacks with E > 64 or H > 8192,
+ *            whose top-k reads z back (EB_ERR_INVALID_ARG there)
  * idx_out    device [T][k] int32
  * w_out      device [T][k] fp32
  * counts_out device [E] int32 (overwritten, not accumulated)
- * Non-finite logits give unspecified (but in-range) picks.
+ * NaN logits rank after every number: a token whose remaining logits are all
+ * NaN takes the lowest expert ids not yet picked, in ascending order (weight
+ * NaN), so every token's k picks are distinct experts.
  */
 int easybalance_route(const eb_model_desc* desc, int32_t layer, int32_t T, const float* x,
                       const float* gain, const void* Wg, const float* bias, void* a_out,
@@ -152,11 +162,34 @@ int easybalance_route(const eb_model_desc* desc, int32_t layer, int32_t T, const
                       void* stream);
 
 /*
+ * Static placement of every layer's experts on the D (virtual) devices, with
+ * replicas: the redundant-expert placement that Section 5 combines with
+ * EasyBalance to show the two are orthogonal (EPLB; the paper's appendix on
+ * redundant experts).  NULL wherever a placement is optional means the
+ * paper's even mapping: E/D contiguous experts per device, device(e) =
+ * e div (E/D).
+ *
+ * copies[(l*E + e)*R + i], i < R, is the device of copy i of expert e at
+ * layer l; an expert has 1..R copies, on distinct devices listed in
+ * ascending order, and the unused entries after them are -1.  An expert's c
+ * routed pairs are split as evenly as possible over its r copies: copy i
+ * carries c div r pairs, plus one if i < c mod r.  Shared experts stay out
+ * of the workload vectors, as without a placement.
+ */
+typedef struct eb_placement {
+  int32_t L, E, D;        /* must equal the model's (checked)                    */
+  int32_t R;              /* copy entries per expert, 1 <= R <= min(D, 64)       */
+  const int32_t* copies;  /* host [L][E][R]                                      */
+} eb_placement;
+
+/*
  * easybalance_schedule -- RunSet_i = Schedule(S_{i-1}, m) of Algorithm 1.
  * Host only, pure, re-entrant; no GPU access.
  *
  * Workload of micro-batch pool_ids[i] (Section 2.3): for device d,
- *   load_i[d] = sum over experts e in [d*E/D, (d+1)*E/D) of counts[i*E + e].
+ *   load_i[d] = sum over experts e in [d*E/D, (d+1)*E/D) of counts[i*E + e]
+ * (placement NULL), or the pairs its experts' copies on d carry under the
+ * placement at the micro-batch's layer pool_layers[i] (see eb_placement).
  * Utilization of a set R (Eq. 3 for one step): U(R) = sum_d W_d / (D max_d W_d)
  * with W = sum_{i in R} load_i; U = 1 if W is all zero.
  *   EB_POLICY_MAXUTIL (Section 4.2): the R with |R| >= min(m, n_pool) of
@@ -177,10 +210,14 @@ int easybalance_route(const eb_model_desc* desc, int32_t layer, int32_t T, const
  * m           >= 1
  * runset_mask host out: bit j set iff micro-batch j runs in this step
  * step_load   host out [D] int64 (nullable): combined workload W of the RunSet
+ * pool_layers host [n_pool] (required with a placement, else ignored): l_j of
+ *             each pool member, 0 <= l_j < placement->L
+ * placement   host (nullable): see eb_placement (E and D must match)
  */
 int easybalance_schedule(int32_t n_pool, const int32_t* pool_ids, const int32_t* counts,
                          int32_t E, int32_t D, int32_t m, int32_t policy,
-                         uint64_t* runset_mask, int64_t* step_load);
+                         uint64_t* runset_mask, int64_t* step_load, const int32_t* pool_layers,
+                         const eb_placement* placement);
 
 /* Workspace bytes easybalance_moe_step needs for these per-entry token
  * counts (host [n_run]), assuming every eb_step_views member is NULL. */
@@ -275,7 +312,8 @@ int easybalance_combine(const eb_model_desc* desc, int32_t n_run, const eb_work*
  *     l_j += 1 for j in RunSet; route those with l_j < L; drop the finished.
  * The results are the ones the same sequence of calls through the other entry
  * points gives.  The only host<->device synchronisation per step is the copy
- * of the pool's expert counts to pinned host memory for the scheduler.
+ * of the pool's expert counts to pinned host memory for the scheduler (a
+ * buffer the calling thread keeps for later passes, freed at thread exit).
  *
  * policy | EB_PASS_DEVICE_SCHEDULE: the same pass with Schedule on the GPU (a
  * one-workgroup kernel at the start of each step, exact integer arithmetic,
@@ -283,7 +321,8 @@ int easybalance_combine(const eb_model_desc* desc, int32_t n_run, const eb_work*
  * from device memory, and the host queueing steps ahead instead of waiting
  * for the counts: it queues only steps that must run (s steps done and a
  * micro-batch L - l layers short need s + L - l in all) and reads a status
- * word the scheduler kernel writes to host-mapped memory.  The call returns
+ * word the scheduler kernel writes to host-mapped memory (256 bytes the
+ * calling thread keeps for later passes, freed at thread exit).  The call returns
  * once the last step is queued (after the records are copied, if any are
  * asked for).  EB_ERR_UNSUPPORTED if D > 64 or, for fp32, E > 64.
  *
@@ -307,6 +346,12 @@ int easybalance_combine(const eb_model_desc* desc, int32_t n_run, const eb_work*
  *              S shared experts of every layer in the RunSet)
  * layer_loads_out host out [N][L][D] (nullable): per-device load of each
  *              micro-batch at each layer, as its routing produced it
+ * placement    host (nullable): static expert placement with replicas (see
+ *              eb_placement) from which every per-device load above and
+ *              every Schedule decision is formed; NULL = E/D contiguous
+ *              experts per device.  The expert computation does not depend on
+ *              it (on one GPU every copy of an expert is the same weights), so
+ *              the hidden states are those of any other schedule.
  * Steps past max_steps are run but not recorded.
  */
 int easybalance_pass_state_size(const eb_model_desc* desc, int32_t N, int32_t T, size_t* bytes);
@@ -316,7 +361,7 @@ int easybalance_run_pass(const eb_model_desc* desc, int32_t N, int32_t T, float*
                          int32_t m, void* state, size_t state_bytes, int32_t max_steps,
                          int32_t* n_steps_out, uint64_t* runsets_out, int32_t* layers_out,
                          int64_t* step_load_out, int32_t* groups_out, int32_t* layer_loads_out,
-                         void* stream);
+                         const eb_placement* placement, void* stream);
 
 /*
  * Kernel timing for measurement.  Between easybalance_profile_begin(mask) and

@@ -56,6 +56,30 @@ class eb_step_views(ctypes.Structure):
                 ("offsets", ctypes.c_void_p)]
 
 
+class eb_placement(ctypes.Structure):
+    _fields_ = [("L", ctypes.c_int32), ("E", ctypes.c_int32), ("D", ctypes.c_int32),
+                ("R", ctypes.c_int32), ("copies", ctypes.c_void_p)]
+
+
+def make_placement(copies, D: int):
+    """copies: int32 array [L][E][R] (device of each copy, ascending, -1
+    padded), or per layer a list over experts of device lists.  Returns the
+    eb_placement struct (it keeps the array alive)."""
+    if not isinstance(copies, np.ndarray):
+        L, E = len(copies), len(copies[0])
+        R = max(len(c) for layer in copies for c in layer)
+        arr = np.full((L, E, R), -1, dtype=np.int32)
+        for l, layer in enumerate(copies):
+            for e, c in enumerate(layer):
+                arr[l, e, :len(c)] = c
+        copies = arr
+    arr = np.ascontiguousarray(copies, dtype=np.int32)
+    L, E, R = arr.shape
+    p = eb_placement(L, E, D, R, arr.ctypes.data)
+    p._keep = arr
+    return p
+
+
 class EasyBalanceError(RuntimeError):
     def __init__(self, fn: str, code: int, msg: str):
         super().__init__(f"{fn} failed with status {code}: {msg}")
@@ -83,7 +107,8 @@ def lib() -> ctypes.CDLL:
     l.easybalance_route.restype = ctypes.c_int
     l.easybalance_route.argtypes = [D, I32, I32, P, P, P, P, P, P, P, P, P, P]
     l.easybalance_schedule.restype = ctypes.c_int
-    l.easybalance_schedule.argtypes = [I32, P, P, I32, I32, I32, I32, U64P, I64P]
+    l.easybalance_schedule.argtypes = [I32, P, P, I32, I32, I32, I32, U64P, I64P, P,
+                                       ctypes.POINTER(eb_placement)]
     l.easybalance_moe_step_workspace_size.restype = ctypes.c_int
     l.easybalance_moe_step_workspace_size.argtypes = [D, I32, P, SZP]
     l.easybalance_moe_step.restype = ctypes.c_int
@@ -97,7 +122,8 @@ def lib() -> ctypes.CDLL:
     l.easybalance_run_pass.argtypes = [D, I32, I32, P, P, P, P, P, P, I32, I32, P, ctypes.c_size_t,
                                        I32, ctypes.POINTER(ctypes.c_int32), U64P,
                                        ctypes.POINTER(ctypes.c_int32), I64P,
-                                       ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32), P]
+                                       ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32),
+                                       ctypes.POINTER(eb_placement), P]
     l.easybalance_pack_weights.restype = ctypes.c_int
     l.easybalance_pack_weights.argtypes = [D, I32, I32, P, P, P]
     l.easybalance_profile_begin.restype = ctypes.c_int
@@ -141,18 +167,23 @@ def easybalance_route(desc, layer, T, x, gain, Wg, bias, a_out, logits_out, idx_
         _ptr(logits_out), _ptr(idx_out), _ptr(w_out), _ptr(counts_out), stream))
 
 
-def easybalance_schedule(pool_ids, counts, E, D, m, policy=EB_POLICY_MAXUTIL, want_load=True):
-    """pool_ids: ascending ids; counts: [len(pool)][E] host ints.
+def easybalance_schedule(pool_ids, counts, E, D, m, policy=EB_POLICY_MAXUTIL, want_load=True,
+                         layers=None, placement=None):
+    """pool_ids: ascending ids; counts: [len(pool)][E] host ints; layers: the
+    pool members' layers (with a placement from make_placement).
     Returns (runset_mask, step_load or None)."""
     ids = np.ascontiguousarray(pool_ids, dtype=np.int32)
     cnt = np.ascontiguousarray(counts, dtype=np.int32).reshape(len(ids), E) if len(ids) else \
         np.zeros((0, E), np.int32)
+    lay = np.ascontiguousarray(layers, dtype=np.int32) if layers is not None else None
     mask = ctypes.c_uint64(0)
     load = np.zeros(D, dtype=np.int64)
     rc = lib().easybalance_schedule(
         len(ids), ids.ctypes.data if len(ids) else None, cnt.ctypes.data if len(ids) else None,
         E, D, m, policy, ctypes.byref(mask),
-        load.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)) if want_load else None)
+        load.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)) if want_load else None,
+        lay.ctypes.data if lay is not None and len(lay) else None,
+        ctypes.byref(placement) if placement is not None else None)
     _check("easybalance_schedule", rc)
     return mask.value, (load if want_load else None)
 
@@ -214,7 +245,7 @@ def easybalance_pass_state_size(desc, N, T) -> int:
 
 
 def easybalance_run_pass(desc, N, T, x, gain, Wg, bias, W_gu, W_dn, policy, m, state, state_bytes,
-                         max_steps=0, record=False, stream=None):
+                         max_steps=0, record=False, stream=None, placement=None):
     """Returns (n_steps, runsets [n], layers [n][N], step_load [n][D], groups [n],
     layer_loads [N][L][D]) when record, else (n_steps, None, None, None, None, None)."""
     n = ctypes.c_int32(0)
@@ -234,7 +265,8 @@ def easybalance_run_pass(desc, N, T, x, gain, Wg, bias, W_gu, W_dn, policy, m, s
     wg, gu, dn = _ptr_array(Wg), _ptr_array(W_gu), _ptr_array(W_dn)
     _check("easybalance_run_pass", lib().easybalance_run_pass(
         ctypes.byref(desc), N, T, _ptr(x), _ptr(gain), wg, _ptr(bias), gu, dn, policy, m,
-        _ptr(state), state_bytes, max_steps if record else 0, ctypes.byref(n), *ptrs, stream))
+        _ptr(state), state_bytes, max_steps if record else 0, ctypes.byref(n), *ptrs,
+        ctypes.byref(placement) if placement is not None else None, stream))
     k = min(n.value, max_steps) if record else 0
     if not record:
         return n.value, None, None, None, None, None

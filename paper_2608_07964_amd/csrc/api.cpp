@@ -306,8 +306,12 @@ int easybalance_route(const eb_model_desc* desc, int32_t layer, int32_t T, const
   if (T < 0) return set_error(EB_ERR_INVALID_ARG, "T=%d < 0", T);
   if (counts_out == nullptr) return set_error(EB_ERR_INVALID_ARG, "counts_out is NULL");
   if (T > 0 && (x == nullptr || gain == nullptr || Wg == nullptr || bias == nullptr ||
-                a_out == nullptr || logits_out == nullptr || idx_out == nullptr || w_out == nullptr))
+                a_out == nullptr || idx_out == nullptr || w_out == nullptr))
     return set_error(EB_ERR_INVALID_ARG, "a required route pointer is NULL");
+  if (T > 0 && logits_out == nullptr && route_logits_required(*desc))
+    return set_error(EB_ERR_INVALID_ARG,
+                     "logits_out is NULL, but this stack's top-k reads the logits back (fp32, E=%d, H=%d)",
+                     desc->E, desc->H);
   return hip_status(launch_route(*desc, T, x, gain, Wg, bias, a_out, logits_out, idx_out, w_out,
                                  counts_out, static_cast<hipStream_t>(stream)),
                     "route launch");
@@ -315,8 +319,9 @@ int easybalance_route(const eb_model_desc* desc, int32_t layer, int32_t T, const
 
 int easybalance_schedule(int32_t n_pool, const int32_t* pool_ids, const int32_t* counts,
                          int32_t E, int32_t D, int32_t m, int32_t policy, uint64_t* runset_mask,
-                         int64_t* step_load) {
-  return schedule_impl(n_pool, pool_ids, counts, E, D, m, policy, runset_mask, step_load);
+                         int64_t* step_load, const int32_t* pool_layers, const eb_placement* placement) {
+  return schedule_impl(n_pool, pool_ids, counts, E, D, m, policy, runset_mask, step_load, pool_layers,
+                       placement);
 }
 
 int easybalance_moe_step_workspace_size(const eb_model_desc* desc, int32_t n_run,
@@ -335,14 +340,24 @@ int easybalance_moe_step(const eb_model_desc* desc, int32_t n_run, const eb_work
                          const void* const* W_gu, const void* const* W_dn, void* ws,
                          size_t ws_bytes, void* o_out, int32_t* inv_out,
                          const eb_step_views* views, void* stream) {
+  return moe_step_common(desc, n_run, run, W_gu, W_dn, ws, ws_bytes, o_out, inv_out, views, stream, false);
+}
+
+}  // extern "C"
+
+namespace eb {
+
+int moe_step_common(const eb_model_desc* desc, int32_t n_run, const eb_work* run, const void* const* W_gu,
+                    const void* const* W_dn, void* ws, size_t ws_bytes, void* o_out, int32_t* inv_out,
+                    const eb_step_views* views, void* stream, bool static_scratch) {
   int rc = check_desc(desc);
   if (rc) return rc;
   rc = check_run(*desc, n_run, run, true);
   if (rc) return rc;
   const eb_model_desc& d = *desc;
-  std::vector<int32_t> Ts(n_run);
+  int32_t Ts[EB_MAX_RUN];  // no heap allocation on this path (n_run <= EB_MAX_RUN, checked)
   for (int i = 0; i < n_run; ++i) Ts[i] = run[i].T;
-  const StepShape sh = step_shape(d, n_run, Ts.data());
+  const StepShape sh = step_shape(d, n_run, Ts);
   if (sh.P == 0) return EB_OK;
   if (W_gu == nullptr || W_dn == nullptr) return set_error(EB_ERR_INVALID_ARG, "W_gu/W_dn is NULL");
   WeightTable wt;
@@ -360,8 +375,12 @@ int easybalance_moe_step(const eb_model_desc* desc, int32_t n_run, const eb_work
   if (ws == nullptr || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0)
     return set_error(EB_ERR_INVALID_ARG, "workspace must be non-NULL and 256-byte aligned");
   const WsLayout L = ws_layout(d, sh, views);
-  if (ws_bytes < L.total)
+  if (ws_bytes < L.total) {
+    if (static_scratch)
+      return set_error(EB_ERR_UNSUPPORTED, "the step needs %zu bytes of scratch, more than the static %zu",
+                       L.total, ws_bytes);
     return set_error(EB_ERR_WORKSPACE_TOO_SMALL, "workspace %zu < %zu bytes", ws_bytes, L.total);
+  }
   const StepWs w = carve_step(d, sh, views, ws, inv_out);
   hipStream_t s = static_cast<hipStream_t>(stream);
 
@@ -378,6 +397,10 @@ int easybalance_moe_step(const eb_model_desc* desc, int32_t n_run, const eb_work
     return rc;
   return run_gemms(d, sh, w, wt, o_out, s);
 }
+
+}  // namespace eb
+
+extern "C" {
 
 int easybalance_combine(const eb_model_desc* desc, int32_t n_run, const eb_work* run,
                         float* const* x_inout, const void* o, const int32_t* inv, void* stream) {

@@ -140,6 +140,9 @@ struct DevPassArgs {
   int32_t* rec_groups;           // [max_records] distinct (layer, expert) groups
   int32_t* rec_layer_loads;      // [N][L][D] per-device load of (j, l), -1 until seen
   unsigned long long* status;    // host-mapped: tag << 48 | steps << 16 | max_j (L - l_j)
+  const int32_t* place;          // [L][E][R] expert copies (eb_placement), or NULL: E/D
+                                 // contiguous experts per device
+  int32_t R;                     // copy entries per expert of place
 };
 
 hipError_t launch_pass_init(const DevPassArgs& A, hipStream_t s);
@@ -155,6 +158,9 @@ hipError_t launch_route_batch(const eb_model_desc& d, const RouteBatch& rb, hipS
 // grids cover max_entries entries of T tokens.  Only for stacks whose
 // routing needs no launch per entry (route_batch_device_ok).
 bool route_batch_device_ok(const eb_model_desc& d);
+// Whether the top-k of this stack reads the logits back from global memory
+// (fp32 stacks off the one-workgroup-per-token path), so z must be stored.
+bool route_logits_required(const eb_model_desc& d);
 hipError_t launch_route_batch_dev(const eb_model_desc& d, const RouteBatch* rb, int max_entries, int T,
                                   hipStream_t s);
 hipError_t launch_route(const eb_model_desc& d, int T, const float* x, const float* gain,
@@ -220,11 +226,24 @@ hipError_t launch_combine_split_dev(const RunTable* rt, int max_tokens, const fl
 void prof_start(int kind, hipStream_t s);
 void prof_stop(int kind, hipStream_t s);
 
+// Body of easybalance_moe_step on workspace ws (api.cpp).  static_scratch:
+// ws is the library's static scratch array (a shortfall is then
+// EB_ERR_UNSUPPORTED instead of EB_ERR_WORKSPACE_TOO_SMALL).
+int moe_step_common(const eb_model_desc* desc, int32_t n_run, const eb_work* run, const void* const* W_gu,
+                    const void* const* W_dn, void* ws, size_t ws_bytes, void* o_out, int32_t* inv_out,
+                    const eb_step_views* views, void* stream, bool static_scratch);
+
 // Host scheduler (schedule.cpp); returns EB_OK or an EB_ERR_* code and sets
 // the message through set_error.
 int schedule_impl(int32_t n_pool, const int32_t* pool_ids, const int32_t* counts, int32_t E,
                   int32_t D, int32_t m, int32_t policy, uint64_t* runset_mask,
-                  int64_t* step_load);
+                  int64_t* step_load, const int32_t* pool_layers, const eb_placement* placement);
+// Checks a placement against the model's L, E, D (EB_OK or EB_ERR_INVALID_ARG).
+int check_placement(const eb_placement* p, int L, int E, int D);
+// out[d] += pairs of counts[E] that device d carries at `layer` (placement
+// NULL: E/D contiguous experts per device; else the even split over each
+// expert's copies, the lower copies taking the remainder).
+void add_device_loads(const int32_t* counts, int E, int D, const eb_placement* p, int layer, int64_t* out);
 int set_error(int code, const char* fmt, ...);
 
 }  // namespace eb

@@ -35,7 +35,7 @@ size_t align_p(size_t v) { return (v + kAlignP - 1) / kAlignP * kAlignP; }
 struct PassLayout {
   size_t a, logits, idx, w, counts, o, inv, ws, ws_bytes;
   // device-scheduled pass: scheduler state, step tables, records (N * L steps)
-  size_t dstate, drt, drb, rec_mask, rec_layers, rec_load, rec_groups, rec_ll;
+  size_t dstate, drt, drb, rec_mask, rec_layers, rec_load, rec_groups, rec_ll, place;
   size_t total;
 };
 
@@ -70,6 +70,8 @@ PassLayout pass_layout(const eb_model_desc& d, int N, int T) {
   p.rec_load = take(sizeof(int64_t) * steps * d.D);
   p.rec_groups = take(sizeof(int32_t) * steps);
   p.rec_ll = take(sizeof(int32_t) * (size_t)N * d.L * d.D);
+  // a placement's copy table, R <= min(D, 64) entries per (layer, expert)
+  p.place = take(sizeof(int32_t) * (size_t)d.L * d.E * std::min(d.D, kDevMaxD));
   p.total = off;
   return p;
 }
@@ -160,7 +162,7 @@ int run_pass_device(const eb_model_desc& d, int N, int T, const PassLayout& P, u
                     const void* const* W_gu, const void* const* W_dn, int policy, int m,
                     int max_steps, int32_t* n_steps_out, uint64_t* runsets_out, int32_t* layers_out,
                     int64_t* step_load_out, int32_t* groups_out, int32_t* layer_loads_out,
-                    hipStream_t s) {
+                    const eb_placement* placement, hipStream_t s) {
   const size_t eb = d.dtype == EB_DTYPE_BF16 ? 2 : 4;
   DevPassArgs A;
   memset(&A, 0, sizeof(A));
@@ -196,6 +198,17 @@ int run_pass_device(const eb_model_desc& d, int N, int T, const PassLayout& P, u
   A.rec_groups = reinterpret_cast<int32_t*>(base + P.rec_groups);
   A.rec_layer_loads = reinterpret_cast<int32_t*>(base + P.rec_ll);
   A.status = t_status.d;
+  if (placement) {
+    // the copy table goes to device memory for the scheduler kernel; the
+    // wait makes the caller's table free for reuse when the call returns
+    int32_t* dplace = reinterpret_cast<int32_t*>(base + P.place);
+    const size_t bytes = sizeof(int32_t) * (size_t)d.L * d.E * placement->R;
+    if (hipMemcpyAsync(dplace, placement->copies, bytes, hipMemcpyHostToDevice, s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess)
+      return set_error(EB_ERR_HIP, "placement copy: %s", hipGetErrorString(hipGetLastError()));
+    A.place = dplace;
+    A.R = placement->R;
+  }
   WeightTable wt;
   memset(&wt, 0, sizeof(wt));
   for (int l = 0; l < d.L; ++l) {
@@ -280,7 +293,7 @@ int easybalance_run_pass(const eb_model_desc* desc, int32_t N, int32_t T, float*
                          int32_t m, void* state, size_t state_bytes, int32_t max_steps,
                          int32_t* n_steps_out, uint64_t* runsets_out, int32_t* layers_out,
                          int64_t* step_load_out, int32_t* groups_out, int32_t* layer_loads_out,
-                         void* stream) {
+                         const eb_placement* placement, void* stream) {
   size_t need = 0;
   int rc = easybalance_pass_state_size(desc, N, T, &need);
   if (rc) return rc;
@@ -307,6 +320,7 @@ int easybalance_run_pass(const eb_model_desc* desc, int32_t N, int32_t T, float*
     return set_error(EB_ERR_WORKSPACE_TOO_SMALL, "state %zu < %zu bytes", state_bytes, need);
   if (max_steps < 0 || ((runsets_out || layers_out || step_load_out || groups_out) && max_steps == 0))
     return set_error(EB_ERR_INVALID_ARG, "max_steps=%d", max_steps);
+  if (placement && (rc = check_placement(placement, d.L, d.E, d.D))) return rc;
 
   const PassLayout P = pass_layout(d, N, T);
   uint8_t* base = static_cast<uint8_t*>(state);
@@ -322,9 +336,6 @@ int easybalance_run_pass(const eb_model_desc* desc, int32_t N, int32_t T, float*
   void* ws = base + P.ws;
   hipStream_t s = static_cast<hipStream_t>(stream);
 
-  int32_t* counts = t_pinned.get((size_t)N * d.E);
-  if (counts == nullptr) return set_error(EB_ERR_HIP, "pinned host allocation failed");
-  const int per = d.E / d.D;
   if (layer_loads_out) {
     for (size_t i = 0; i < (size_t)N * d.L * d.D; ++i) layer_loads_out[i] = -1;
   }
@@ -357,9 +368,12 @@ int easybalance_run_pass(const eb_model_desc* desc, int32_t N, int32_t T, float*
   if ((rc = route(pool))) return rc;
   if (device)
     return run_pass_device(d, N, T, P, base, x, gain, Wg, bias, W_gu, W_dn, policy, m, max_steps, n_steps_out,
-                           runsets_out, layers_out, step_load_out, groups_out, layer_loads_out, s);
-  std::vector<int32_t> pool_counts;
-  std::vector<int64_t> load(d.D);
+                           runsets_out, layers_out, step_load_out, groups_out, layer_loads_out, placement, s);
+  // host-scheduled: the pool's counts come back through this thread's pinned buffer
+  int32_t* counts = t_pinned.get((size_t)N * d.E);
+  if (counts == nullptr) return set_error(EB_ERR_HIP, "pinned host allocation failed");
+  std::vector<int32_t> pool_counts, pool_layers;
+  std::vector<int64_t> load(d.D), lj(d.D);
   std::vector<eb_work> run;
   std::vector<float*> xs;
   int n_steps = 0;
@@ -369,26 +383,29 @@ int easybalance_run_pass(const eb_model_desc* desc, int32_t N, int32_t T, float*
       return set_error(EB_ERR_HIP, "counts copy: %s", hipGetErrorString(hipGetLastError()));
     const int n_pool = (int)pool.size();
     if (layer_loads_out) {
-      for (int j : pool)
-        for (int dv = 0; dv < d.D; ++dv) {
-          int64_t sum = 0;
-          for (int e = dv * per; e < (dv + 1) * per; ++e) sum += counts[(size_t)j * d.E + e];
-          layer_loads_out[((size_t)j * d.L + layer[j]) * d.D + dv] = (int32_t)sum;
-        }
+      for (int j : pool) {
+        std::fill(lj.begin(), lj.end(), 0);
+        add_device_loads(counts + (size_t)j * d.E, d.E, d.D, placement, layer[j], lj.data());
+        for (int dv = 0; dv < d.D; ++dv)
+          layer_loads_out[((size_t)j * d.L + layer[j]) * d.D + dv] = (int32_t)lj[dv];
+      }
     }
     uint64_t mask = 0;
     if (policy == EB_POLICY_LOCKSTEP) {
       for (int dv = 0; dv < d.D; ++dv) load[dv] = 0;
       for (int j : pool) {
         mask |= 1ull << j;
-        for (int e = 0; e < d.E; ++e) load[e / per] += counts[(size_t)j * d.E + e];
+        add_device_loads(counts + (size_t)j * d.E, d.E, d.D, placement, layer[j], load.data());
       }
     } else {
       pool_counts.resize((size_t)n_pool * d.E);
-      for (int i = 0; i < n_pool; ++i)
+      pool_layers.resize(n_pool);
+      for (int i = 0; i < n_pool; ++i) {
         memcpy(&pool_counts[(size_t)i * d.E], counts + (size_t)pool[i] * d.E, sizeof(int32_t) * d.E);
+        pool_layers[i] = layer[pool[i]];
+      }
       if ((rc = schedule_impl(n_pool, pool.data(), pool_counts.data(), d.E, d.D, m, policy, &mask,
-                              load.data())))
+                              load.data(), pool_layers.data(), placement)))
         return rc;
     }
     run.clear();

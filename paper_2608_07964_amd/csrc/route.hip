@@ -98,10 +98,12 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(RBA rba, int H, float eps)
 // ---------------------------------------------------------------------------
 // Top-k and softmax weights of one token by one thread.  zrow(e) gives the
 // token's logits e < E.  The picks are kept as a list ordered by the total
-// order "larger z first, then lower expert id" (NaN is never picked; a slot
-// that nothing can fill takes expert E-1), built by one ascending pass over e
-// with compare-and-swap insertion; the softmax maximum and denominator are
-// accumulated over e in ascending order.
+// order "larger z first, then lower expert id", built by one ascending pass
+// over e with compare-and-swap insertion; NaN never enters the list, so a
+// slot left empty means every expert not yet picked has a NaN logit, and it
+// takes the lowest such id (NaN ranks after every number, ties by id: the
+// k picks are always distinct experts).  The softmax maximum and denominator
+// are accumulated over e in ascending order.
 __device__ __forceinline__ bool better(float v1, int e1, float v2, int e2) {
   return v1 > v2 || (v1 == v2 && e1 < e2);
 }
@@ -142,10 +144,23 @@ __device__ __forceinline__ void topk_thread(int E, int k, int norm_topk, ZRow zr
     esum += ev[j];
   }
   const float denom = norm_topk ? esum : se;
+  int fill = 0;  // candidate for the next empty slot (ids ascending)
 #pragma unroll
   for (int j = 0; j < KMAX; ++j) {
     if (j < k) {
-      idx_t[j] = le[j] < E ? le[j] : E - 1;
+      int e = le[j];
+      if (e >= E) {
+        for (;; ++fill) {
+          bool used = false;
+#pragma unroll
+          for (int i = 0; i < KMAX; ++i) used |= i < j && le[i] == fill;
+          if (!used || fill >= E - 1) break;
+        }
+        e = fill++;
+        le[j] = e;
+        ev[j] = __builtin_nanf("");
+      }
+      idx_t[j] = e;
       w_t[j] = ev[j] / denom;
     }
   }
@@ -218,7 +233,18 @@ __device__ __forceinline__ void topk_group8(int sub, int E, int k, int norm_topk
           be = oe;
         }
       }
-      if (be >= E) be = E - 1;  // only when every remaining logit is NaN
+      if (be >= E) {
+        // every expert not yet picked has a NaN logit: the lowest such id
+        // (NaN ranks after every number, ties by id)
+        int lo = E;
+#pragma unroll
+        for (int i = PER - 1; i >= 0; --i)
+          if (!(taken & (1u << i))) lo = sub + 8 * i;
+#pragma unroll
+        for (int off = 1; off < 8; off <<= 1) lo = min(lo, __shfl_xor(lo, off, 8));
+        be = min(lo, E - 1);
+        bv = __builtin_nanf("");
+      }
       if ((be & 7) == sub) taken |= 1u << (be >> 3);
       const float ev = expf(bv - mx);
       esum += ev;
@@ -439,7 +465,7 @@ __global__ __launch_bounds__(256) void route_token_kernel(RBA rba, int H, int E,
   if (tid < E) {
     const float ze = (((red_z[0][tid] + red_z[1][tid]) + red_z[2][tid]) + red_z[3][tid]) + bias[tid];
     red_z[0][tid] = ze;  // each thread rewrites only its own entry
-    z[(size_t)t * E + tid] = ze;
+    if (z != nullptr) z[(size_t)t * E + tid] = ze;
   }
   __syncthreads();
   if (tid == 0)
@@ -541,7 +567,7 @@ __global__ __launch_bounds__(256) void route_mfma_kernel(RBA rba, int H, int E, 
         if (e < E) {
           const float ze = sum + bias[e];
           zs[tl][e] = ze;
-          if (t0 + tl < T) z[(size_t)(t0 + tl) * E + e] = ze;
+          if (z != nullptr && t0 + tl < T) z[(size_t)(t0 + tl) * E + e] = ze;
         }
       }
     }
@@ -650,6 +676,10 @@ hipError_t launch_route_batch(const eb_model_desc& d, const RouteBatch& rb, hipS
   if (d.dtype == EB_DTYPE_BF16)
     return route_batch_typed<bf16_t>(d, a, &rb, rb.n, rb.tok0[rb.n], rb.blk0[rb.n], s);
   return route_batch_typed<float>(d, a, &rb, rb.n, rb.tok0[rb.n], rb.blk0[rb.n], s);
+}
+
+bool route_logits_required(const eb_model_desc& d) {
+  return d.dtype != EB_DTYPE_BF16 && !fused_token_path<float>(d);
 }
 
 bool route_batch_device_ok(const eb_model_desc& d) {

@@ -240,9 +240,25 @@ __global__ __launch_bounds__(kSchedThreads) void sched_step_kernel(DevPassArgs A
       const int i = i0 + u * kSchedThreads;
       if (i < n * E && c[u] != 0) {
         const int pi = i / E, e = i - pi * E;
-        atomicAdd(reinterpret_cast<unsigned long long*>(&s_load[pi * kDevMaxD + e / per]),
-                  (unsigned long long)c[u]);
-        atomicAdd(reinterpret_cast<unsigned long long*>(&s_tot[e / per]), (unsigned long long)c[u]);
+        if (A.place == nullptr) {
+          atomicAdd(reinterpret_cast<unsigned long long*>(&s_load[pi * kDevMaxD + e / per]),
+                    (unsigned long long)c[u]);
+          atomicAdd(reinterpret_cast<unsigned long long*>(&s_tot[e / per]), (unsigned long long)c[u]);
+        } else {
+          // the expert's pairs split evenly over its copies (validated on the
+          // host: 1..R distinct devices < D, ascending, then -1), the lower
+          // copies taking the remainder
+          const int32_t* cp = A.place + ((size_t)s_layer[s_pool[pi]] * E + e) * A.R;
+          int r = 1;
+          while (r < A.R && cp[r] >= 0) ++r;
+          const int q = c[u] / r, rem = c[u] - q * r;
+          for (int ci = 0; ci < r; ++ci) {
+            const int dv = cp[ci];
+            const unsigned long long share = (unsigned long long)(q + (ci < rem ? 1 : 0));
+            atomicAdd(reinterpret_cast<unsigned long long*>(&s_load[pi * kDevMaxD + dv]), share);
+            atomicAdd(reinterpret_cast<unsigned long long*>(&s_tot[dv]), share);
+          }
+        }
         atomicOr(&s_nz[i >> 5], 1u << (i & 31));
       }
     }

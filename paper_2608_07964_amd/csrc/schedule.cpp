@@ -177,9 +177,52 @@ uint64_t diffpeak(int n, const std::vector<int64_t>& load, int D, int need) {
 
 }  // namespace
 
+int check_placement(const eb_placement* p, int L, int E, int D) {
+  if (p->L != L || p->E != E || p->D != D)
+    return set_error(EB_ERR_INVALID_ARG, "placement is for L=%d E=%d D=%d, not L=%d E=%d D=%d", p->L, p->E,
+                     p->D, L, E, D);
+  if (p->R < 1 || p->R > D || p->R > kDevMaxD)
+    return set_error(EB_ERR_INVALID_ARG, "placement R=%d outside [1, min(D=%d, %d)]", p->R, D, kDevMaxD);
+  if (p->copies == nullptr) return set_error(EB_ERR_INVALID_ARG, "placement copies is NULL");
+  for (int l = 0; l < L; ++l)
+    for (int e = 0; e < E; ++e) {
+      const int32_t* c = p->copies + ((size_t)l * E + e) * p->R;
+      if (c[0] < 0 || c[0] >= D)
+        return set_error(EB_ERR_INVALID_ARG, "placement: expert %d of layer %d has no copy on a device", e, l);
+      bool ended = false;
+      for (int i = 1; i < p->R; ++i) {
+        if (c[i] < 0) {
+          if (c[i] != -1) return set_error(EB_ERR_INVALID_ARG, "placement: entry %d of (%d, %d) is %d", i, l, e, c[i]);
+          ended = true;
+        } else if (ended || c[i] >= D || c[i] <= c[i - 1]) {
+          return set_error(EB_ERR_INVALID_ARG,
+                           "placement: copies of expert %d at layer %d must be distinct devices < %d, ascending, "
+                           "then -1", e, l, D);
+        }
+      }
+    }
+  return EB_OK;
+}
+
+void add_device_loads(const int32_t* counts, int E, int D, const eb_placement* p, int layer, int64_t* out) {
+  if (p == nullptr) {
+    const int per = E / D;
+    for (int e = 0; e < E; ++e) out[e / per] += counts[e];
+    return;
+  }
+  const int32_t* row = p->copies + (size_t)layer * E * p->R;
+  for (int e = 0; e < E; ++e) {
+    const int32_t* c = row + (size_t)e * p->R;
+    int r = 1;
+    while (r < p->R && c[r] >= 0) ++r;
+    const int64_t q = counts[e] / r, rem = counts[e] % r;
+    for (int i = 0; i < r; ++i) out[c[i]] += q + (i < rem ? 1 : 0);
+  }
+}
+
 int schedule_impl(int32_t n_pool, const int32_t* pool_ids, const int32_t* counts, int32_t E,
                   int32_t D, int32_t m, int32_t policy, uint64_t* runset_mask,
-                  int64_t* step_load) {
+                  int64_t* step_load, const int32_t* pool_layers, const eb_placement* placement) {
   if (runset_mask == nullptr) return set_error(EB_ERR_INVALID_ARG, "runset_mask is NULL");
   if (n_pool < 0 || n_pool > EB_MAX_POOL)
     return set_error(EB_ERR_INVALID_ARG, "n_pool=%d outside [0, %d]", n_pool, EB_MAX_POOL);
@@ -196,6 +239,16 @@ int schedule_impl(int32_t n_pool, const int32_t* pool_ids, const int32_t* counts
     if (i > 0 && pool_ids[i] <= pool_ids[i - 1])
       return set_error(EB_ERR_INVALID_ARG, "pool_ids must be strictly ascending");
   }
+  if (placement != nullptr) {
+    const int rc = check_placement(placement, placement->L, E, D);
+    if (rc) return rc;
+    if (n_pool > 0 && pool_layers == nullptr)
+      return set_error(EB_ERR_INVALID_ARG, "pool_layers is NULL (required with a placement)");
+    for (int i = 0; i < n_pool; ++i)
+      if (pool_layers[i] < 0 || pool_layers[i] >= placement->L)
+        return set_error(EB_ERR_INVALID_ARG, "pool_layers[%d]=%d outside [0, %d)", i, pool_layers[i],
+                         placement->L);
+  }
   if (policy == EB_POLICY_MAXUTIL && n_pool > EB_MAXUTIL_MAX_POOL)
     return set_error(EB_ERR_UNSUPPORTED, "MaxUtil enumerates up to 2^n subsets; n_pool=%d > %d",
                      n_pool, EB_MAXUTIL_MAX_POOL);
@@ -204,14 +257,13 @@ int schedule_impl(int32_t n_pool, const int32_t* pool_ids, const int32_t* counts
     if (step_load) memset(step_load, 0, sizeof(int64_t) * (size_t)D);
     return EB_OK;
   }
-  const int per = E / D;
   std::vector<int64_t> load((size_t)n_pool * D, 0);
-  for (int i = 0; i < n_pool; ++i)
-    for (int e = 0; e < E; ++e) {
-      const int32_t c = counts[(size_t)i * E + e];
-      if (c < 0) return set_error(EB_ERR_INVALID_ARG, "negative count at [%d][%d]", i, e);
-      load[(size_t)i * D + e / per] += c;
-    }
+  for (int i = 0; i < n_pool; ++i) {
+    for (int e = 0; e < E; ++e)
+      if (counts[(size_t)i * E + e] < 0) return set_error(EB_ERR_INVALID_ARG, "negative count at [%d][%d]", i, e);
+    add_device_loads(counts + (size_t)i * E, E, D, placement, placement ? pool_layers[i] : 0,
+                     load.data() + (size_t)i * D);
+  }
   const int need = m < n_pool ? m : n_pool;
   uint64_t set;
   if (policy == EB_POLICY_MAXUTIL)

@@ -115,11 +115,13 @@ class Stack:
 
     # ---- Algorithm 1, natively ----------------------------------------------
     def run_native(self, policy: str = "maxutil", m: int | None = None, record: bool = True,
-                   stream=None, device_schedule: bool = False) -> list[StepRecord]:
+                   stream=None, device_schedule: bool = False, placement=None) -> list[StepRecord]:
         """The same pass as run(), driven by easybalance_run_pass (the host
         loop in the library; device_schedule: Schedule on the GPU, the host
         queueing steps ahead).  Fills layer_loads and returns the steps when
-        record (records cover the first N*L steps, i.e. all of them)."""
+        record (records cover the first N*L steps, i.e. all of them).
+        placement: a binding.make_placement struct (static expert placement
+        with replicas) from which the loads and decisions are formed."""
         if stream is None:
             stream = torch.cuda.current_stream(self.dev)
         pol = B.EB_POLICY_LOCKSTEP if policy == "lockstep" else POLICIES[policy]
@@ -133,7 +135,7 @@ class Stack:
         n, rs, ly, sl, gr, ll = B.easybalance_run_pass(
             self.desc, self.N, self.T, self.x, self.gain, self.Wg, self.bias, self.W_gu, self.W_dn,
             pol, m, sp, self._state_bytes, max_steps=self.N * self.L, record=record,
-            stream=stream.cuda_stream)
+            stream=stream.cuda_stream, placement=placement)
         if not record:
             return []
         self.layer_loads = ll.astype(np.int64)

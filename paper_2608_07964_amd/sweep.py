@@ -3,7 +3,8 @@ micro-batches N, minimum combination size m and number of virtual devices
 D (the studies of Section 5: scheduling strategies, micro-batch count and
 m, EP size, and the worst-case statistic of Section 4.1), EasyBalance on top
 of a static replicated expert placement (the orthogonality study of Section 5
-and the appendix on redundant experts), and the scheduler's cost per step
+and the appendix on redundant experts; the library forms the placed loads and
+the decisions itself), and the scheduler's cost per step
 (the context of Table 3), on the synthetic stacks.
 
 The stacks are MoE-only (x <- x + MoE_l(RMSNorm(x))), so a token's hidden
@@ -123,28 +124,55 @@ def replicated_placement(hist, D: int, replicas: int, first_device: int = 0) -> 
     return [sorted(s) for s in slots]
 
 
-def placed_loads(counts: np.ndarray, placements) -> np.ndarray:
-    """Per-device load w[j][l][d] under per-layer placements (placements[l] =
-    slots as from replicated_placement): expert e's pairs are split evenly
-    over its copies, the first c mod r copies in device order taking one
-    more."""
-    counts = np.asarray(counts, dtype=np.int64)
+def run_policy_counts(counts: np.ndarray, D: int, policy: str, m: int, placement=None) -> list[np.ndarray]:
+    """Per-device workload of every executed step of one pass of Algorithm 1
+    replayed with the library's scheduler on per-expert counts c[j][l][e]:
+    the loads come from easybalance_schedule itself, under `placement` (a
+    binding.make_placement struct: static placement with replicas) or, when
+    it is None, the contiguous E/D mapping.  lockstep: step l runs every
+    micro-batch at layer l (the scheduler asked for the whole pool);
+    separate: every (j, l) alone."""
+    counts = np.asarray(counts, np.int64)
     N, L, E = counts.shape
-    D = len(placements[0])
-    out = np.zeros((N, L, D), dtype=np.int64)
-    for layer in range(L):
-        holders = [[] for _ in range(E)]
-        for d, held in enumerate(placements[layer]):
-            for e in held:
-                holders[e].append(d)
-        if any(not h for h in holders):
-            raise ValueError(f"layer {layer}: an expert has no device")
-        for e in range(E):
-            r = len(holders[e])
-            c = counts[:, layer, e]
-            for i, d in enumerate(holders[e]):
-                out[:, layer, d] += c // r + (c % r > i)
-    return out
+    if counts.max(initial=0) > np.iinfo(np.int32).max:
+        raise ValueError("counts exceed int32")
+    if policy == "separate":
+        steps = []
+        for layer in range(L):
+            for j in range(N):
+                _, load = B.easybalance_schedule([j], counts[[j], layer], E, D, 1, B.EB_POLICY_MAXUTIL,
+                                                 layers=[layer], placement=placement)
+                steps.append(load.copy())
+        return steps
+    layer = np.zeros(N, dtype=np.int64)
+    pool = list(range(N))
+    steps = []
+    while pool:
+        cur = counts[pool, layer[pool]]
+        if policy == "lockstep":
+            pol, mm = B.EB_POLICY_MAXUTIL, len(pool)     # the only candidate: the whole pool
+        else:
+            pol, mm = _NATIVE[policy], m
+        mask, load = B.easybalance_schedule(pool, cur, E, D, mm, pol, layers=layer[pool], placement=placement)
+        R = [j for j in pool if (mask >> j) & 1]
+        if not R:
+            raise RuntimeError("scheduler returned an empty run set")
+        steps.append(load.copy())
+        layer[R] += 1
+        pool = [j for j in pool if layer[j] < L]
+    return steps
+
+
+def placement_copies(slots, E: int) -> list[list[int]]:
+    """Per expert, the devices holding a copy (ascending), from a layer's
+    slots[d] (the experts device d holds)."""
+    holders = [[] for _ in range(E)]
+    for d, held in enumerate(slots):
+        for e in held:
+            holders[e].append(d)
+    if any(not h for h in holders):
+        raise ValueError("an expert has no device")
+    return holders
 
 
 def run_policy(loads: np.ndarray, policy: str, m: int) -> list[np.ndarray]:
@@ -251,19 +279,20 @@ def report(routes: np.ndarray, cfg) -> str:
     # Ties at device 0 in every layer put every layer's hottest expert on one
     # device (its peaks coincide: the worst case of Section 4.1); rotating the
     # tie order by layer does not.
-    mappings = [("contiguous, E/D experts per device", cfg.E, layer_loads(routes, cfg.N, cfg.E, cfg.D))]
+    mappings = [("contiguous, E/D experts per device", None)]
     for reps in (0, cfg.D):
         for rot in (False, True):
             pl = [replicated_placement(hist[layer], cfg.D, reps, layer % cfg.D if rot else 0)
                   for layer in range(cfg.L)]
             ties = "ties rotated by layer" if rot else "ties at device 0"
             mappings.append((f"placed from history, {cfg.E + reps} physical experts, {ties}",
-                             cfg.E + reps, placed_loads(counts, pl)))
+                             B.make_placement([placement_copies(s, cfg.E) for s in pl], cfg.D)))
     rows = []
-    for name, _, w in mappings:
+    for name, placement in mappings:
         r = {"mapping": name}
         for pol in ("lockstep", "maxutil", "cumutil", "diffpeak"):
-            r[pol] = metrics.summary(run_policy(w, pol, m_def(cfg.N)))["idle_fraction"]
+            r[pol] = metrics.summary(run_policy_counts(counts, cfg.D, pol, m_def(cfg.N),
+                                                       placement))["idle_fraction"]
         rows.append(r)
     parts.append(f"\nStatic placement + EasyBalance (N = {cfg.N}, D = {cfg.D}, m = {m_def(cfg.N)}; "
                  "under-utilization):\n")
@@ -271,7 +300,7 @@ def report(routes: np.ndarray, cfg) -> str:
                         lambda r: [r["mapping"]] + [f"{r[p]:.3f}" for p in
                                                     ("lockstep", "maxutil", "cumutil", "diffpeak")]))
     # scheduler cost per decision at the stack's own N, D, m
-    w = mappings[0][2]
+    w = layer_loads(routes, cfg.N, cfg.E, cfg.D)
     cost = []
     for pol in ("maxutil", "cumutil", "diffpeak"):
         t0 = time.perf_counter()

@@ -217,3 +217,60 @@ def test_empty_step_enqueues_nothing():
     with pytest.raises(B.EasyBalanceError) as ei:
         B.easybalance_moe_step(d, bad, 1, [None, None], [None, None], None, 0, None, None)
     assert ei.value.code == B.EB_ERR_INVALID_ARG
+
+
+def _random_placement(rng, L, E, D):
+    R = int(rng.integers(1, D + 1))
+    copies = [[sorted(rng.choice(D, size=int(rng.integers(1, R + 1)), replace=False).tolist())
+               for _ in range(E)] for _ in range(L)]
+    return copies
+
+
+@pytest.mark.parametrize("policy", [osched.MAXUTIL, osched.CUMUTIL, osched.DIFFPEAK])
+def test_schedule_on_a_replicated_placement_matches_oracle(policy):
+    """Section 5's orthogonality study: Schedule on the loads of a static
+    placement with replicas equals the oracle's choice on the oracle's placed
+    loads of each pool member at its own layer."""
+    rng = np.random.default_rng(60 + policy)
+    for trial in range(400):
+        n = int(rng.integers(1, 9))
+        D = int(rng.choice([1, 2, 3, 4, 8]))
+        E = D * int(rng.integers(1, 4))
+        L = int(rng.integers(1, 5))
+        m = int(rng.integers(1, n + 2))
+        ids = sorted(rng.choice(64, size=n, replace=False).tolist())
+        layers = rng.integers(0, L, size=n).tolist()
+        copies = _random_placement(rng, L, E, D)
+        counts = rng.integers(0, int(rng.choice([3, 50])), size=(n, E)).astype(np.int32)
+        pl = B.make_placement(copies, D)
+        mask, load = B.easybalance_schedule(ids, counts, E, D, m, POL[policy], layers=layers, placement=pl)
+        loads = {j: omodel.placed_device_loads(counts[i], copies[layers[i]], D) for i, j in enumerate(ids)}
+        want = osched.schedule(ids, loads, D, m, policy)
+        got = tuple(j for j in ids if (mask >> j) & 1)
+        assert got == want, (ids, layers, copies, counts.tolist(), D, m)
+        assert np.array_equal(load, sum(loads[j] for j in want))
+
+
+def test_placement_argument_checks():
+    E, D, L = 4, 2, 2
+    ids, counts = [0, 1], np.ones((2, E), np.int32)
+    good = [[[0], [0, 1], [1], [1]]] * L
+    B.easybalance_schedule(ids, counts, E, D, 1, layers=[0, 1], placement=B.make_placement(good, D))
+    bad = {
+        "no copy": np.array([[[0, -1], [-1, -1], [1, -1], [1, -1]]] * L),
+        "device out of range": np.array([[[0, -1], [2, -1], [1, -1], [1, -1]]] * L),
+        "not ascending": np.array([[[1, 0], [0, -1], [1, -1], [1, -1]]] * L),
+        "repeated device": np.array([[[0, 0], [0, -1], [1, -1], [1, -1]]] * L),
+        "hole": np.array([[[0, -1], [-1, 1], [1, -1], [1, -1]]] * L),
+    }
+    for what, arr in bad.items():
+        with pytest.raises(B.EasyBalanceError) as ei:
+            B.easybalance_schedule(ids, counts, E, D, 1, layers=[0, 1], placement=B.make_placement(arr, D))
+        assert ei.value.code == B.EB_ERR_INVALID_ARG, what
+    pl = B.make_placement(good, D)
+    with pytest.raises(B.EasyBalanceError):          # layers are required with a placement
+        B.easybalance_schedule(ids, counts, E, D, 1, placement=pl)
+    with pytest.raises(B.EasyBalanceError):          # a layer the placement does not cover
+        B.easybalance_schedule(ids, counts, E, D, 1, layers=[0, 2], placement=pl)
+    with pytest.raises(B.EasyBalanceError):          # made for another E
+        B.easybalance_schedule(ids, np.ones((2, 6), np.int32), 6, D, 1, layers=[0, 1], placement=pl)

@@ -65,3 +65,72 @@ def test_native_pass_pool_over_32_micro_batches(device):
     cfg = mini(BY_NAME["qwen_moe_bf16"], N=40, T=24, L=2)
     assert cfg.N == 40
     _compare(cfg, device, [("cumutil", 30), ("diffpeak", 30), ("lockstep", None)])
+
+
+def _record_counts(st):
+    """Per-expert counts c[j][l][e] the GPU routing produced, from one
+    lock-step pass of the Python driver (a token's experts do not depend on
+    the schedule: the stacks are MoE-only and the kernels batch invariant)."""
+    counts = np.full((st.N, st.L, st.E), -1, dtype=np.int64)
+
+    def hook(stage, runset):
+        if stage == "pre":
+            c = st.counts.cpu().numpy()
+            for j, layer in runset:
+                counts[j, layer] = c[j]
+
+    st.run("lockstep", record=False, hook=hook)
+    torch.cuda.synchronize()
+    assert (counts >= 0).all()
+    return counts
+
+
+@pytest.mark.parametrize("name", ["mixtral_bf16", "qwen_moe_bf16", "dsv2_lite_bf16"])
+def test_native_pass_on_replicated_placement(name, device):
+    """EasyBalance on a static placement with replicas (Section 5, orthogonality
+    with EPLB) through the library, host- and device-scheduled: the recorded
+    per-device loads are the oracle's placed loads of the GPU's counts, every
+    executed schedule is the oracle's Algorithm-1 replay on them, each step's
+    workload is the oracle's, and the hidden states equal the lock-step pass's
+    bit for bit."""
+    from oracle import metrics as ometrics
+    from oracle import model as omodel
+    from oracle import sched as osched
+    from paper_2608_07964_amd import binding as B
+    from paper_2608_07964_amd import sweep
+
+    cfg = mini(BY_NAME[name])
+    log(f"placement {cfg.name}")
+    inp = DeviceInputs(cfg, device)
+    st, _ = make_stack(cfg, device, inputs=inp)
+    counts = _record_counts(st)
+    x_ref = st.x.clone()
+    # an EPLB-like placement from the batch's own history: D extra copies of
+    # the hottest experts, and a random one with up to 3 copies per expert
+    rng = np.random.default_rng(77)
+    hist = counts.sum(axis=0)
+    placements = {
+        "history": [sweep.placement_copies(sweep.replicated_placement(hist[l], cfg.D, cfg.D, l % cfg.D), cfg.E)
+                    for l in range(cfg.L)],
+        "random": [[sorted(rng.choice(cfg.D, size=int(rng.integers(1, min(3, cfg.D) + 1)), replace=False).tolist())
+                    for _ in range(cfg.E)] for _ in range(cfg.L)],
+    }
+    pols = {"maxutil": osched.MAXUTIL, "cumutil": osched.CUMUTIL, "diffpeak": osched.DIFFPEAK}
+    for pname, copies in placements.items():
+        placed = np.stack([omodel.placed_device_loads(counts[:, l], copies[l], cfg.D) for l in range(cfg.L)],
+                          axis=1)
+        pl = B.make_placement(copies, cfg.D)
+        for policy, m in [("maxutil", cfg.m), ("cumutil", cfg.m), ("diffpeak", cfg.m), ("lockstep", None)]:
+            for dev_sched in (False, True):
+                st.x.copy_(inp.x0)
+                steps = st.run_native(policy, m=m, device_schedule=dev_sched, placement=pl)
+                torch.cuda.synchronize()
+                what = (pname, policy, m, "device" if dev_sched else "host")
+                assert np.array_equal(st.layer_loads, placed), what
+                want = (osched.lockstep_steps(cfg.N, cfg.L) if policy == "lockstep"
+                        else osched.run_algorithm1(placed, m, pols[policy]))
+                assert [s.runset for s in steps] == want, what
+                for s in steps:
+                    assert np.array_equal(s.load, ometrics.step_workload(placed, s.runset)), what
+                assert torch.equal(st.x, x_ref), what
+        log(f"  {cfg.name} {pname}: every policy matches the oracle on the placed loads")

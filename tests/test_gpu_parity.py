@@ -326,3 +326,49 @@ def test_moe_step_group_sizes_span_tile_shapes(device):
         assert_close(h_gpu[r0:r1], h_ref, cfg.dtype, f"h rows={r1 - r0}")
         o_ref = cast(h_gpu[r0:r1] @ np.asarray(P.down(l, e), np.float64).T)
         assert_close(o_gpu[r0:r1], o_ref, cfg.dtype, f"o rows={r1 - r0}")
+
+
+@pytest.mark.parametrize("name", ["mixtral_bf16", "qwen_moe_bf16", "dsv3_share_bf16", "tiny_f32"])
+def test_route_nan_logits_pick_distinct_experts(name, device):
+    """NaN logits rank after every number: with NaN in the router bias of all
+    but a few experts, and with whole NaN rows of x, every token's picks are
+    the oracle's stable top-k of the GPU's own logits (NaN last, ids
+    ascending) -- k distinct experts -- and the counts follow them.  Covers
+    the one-workgroup-per-token router (E <= 8), the matrix-core router with
+    8 lanes per token (E = 60, 256) and the fp32 path; logits_out is also
+    left NULL once, which changes none of the other outputs."""
+    B = _binding()
+    cfg = BY_NAME[name] if name == "tiny_f32" else mini(BY_NAME[name])
+    log(f"route NaN {cfg.name}")
+    inp = DeviceInputs(cfg, device, weights=False)
+    desc = B.make_desc(cfg.L, cfg.H, cfg.F, cfg.E, cfg.k, cfg.S, cfg.D, cfg.dtype, cfg.eps)
+    tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    T = min(cfg.T, 96)
+    x = inp.x0[0, :T].clone()
+    x[5] = float("nan")
+    x[T - 1, 3] = float("nan")                  # one NaN element poisons the row
+    bias = inp.bias[0].clone()
+    keep = [cfg.E - 1, cfg.E // 3] if cfg.k > 1 else [cfg.E // 3]
+    nan_mask = torch.ones(cfg.E, dtype=torch.bool, device=device)
+    nan_mask[keep] = False
+    bias[nan_mask] = float("nan")
+    outs = []
+    for with_z in (True, False):
+        a = torch.empty(T, cfg.H, dtype=tdt, device=device)
+        z = torch.empty(T, cfg.E, dtype=torch.float32, device=device)
+        idx = torch.empty(T, cfg.k, dtype=torch.int32, device=device)
+        w = torch.empty(T, cfg.k, dtype=torch.float32, device=device)
+        counts = torch.empty(cfg.E, dtype=torch.int32, device=device)
+        B.easybalance_route(desc, 0, T, x, inp.g[0], inp.Wg[0], bias, a, z if with_z else None, idx, w, counts)
+        torch.cuda.synchronize()
+        outs.append((z.cpu().numpy(), idx.cpu().numpy(), w.cpu().numpy(), counts.cpu().numpy()))
+    (z, idx, w, counts), (_, idx2, w2, counts2) = outs
+    assert np.isnan(z[5]).all() and np.isnan(z[T - 1]).all()
+    assert np.isnan(z[:, nan_mask.cpu().numpy()]).all()
+    want = omodel.topk_indices(z.astype(np.float64), cfg.k)
+    assert np.array_equal(idx, want)
+    assert all(len(set(r)) == cfg.k for r in idx.tolist())
+    assert np.array_equal(counts, omodel.expert_counts(idx, cfg.E))
+    assert np.array_equal(idx2, idx) and np.array_equal(counts2, counts)
+    assert np.array_equal(np.isnan(w), np.isnan(w2)) and np.array_equal(w[~np.isnan(w)], w2[~np.isnan(w2)])
+    assert np.isnan(w[5]).all()

@@ -5,8 +5,11 @@ hand-worked loads."""
 import numpy as np
 import pytest
 
+from oracle import metrics as ometrics
+from oracle import model as omodel
 from oracle import sched as osched
-from paper_2608_07964_amd import sweep
+from paper_2608_07964_amd import binding as B
+from paper_2608_07964_amd import metrics, sweep
 
 
 def _routes(rng, tokens, L, k, E):
@@ -117,22 +120,36 @@ def test_replicated_placement_invariants():
                 assert len(set(s)) == len(s)
 
 
-def test_placed_loads_split_and_contiguous_case():
+def test_placed_replay_through_the_library_matches_the_oracle():
+    """The placement table of the report comes from the library: the step
+    loads easybalance_schedule forms under a replicated placement equal the
+    oracle's placed loads (Section 5's orthogonality study) replayed by the
+    oracle's Algorithm 1, for every policy; the contiguous placement written
+    out as one copy per expert gives the layer_loads replay."""
     rng = np.random.default_rng(9)
     r = _routes(rng, 32, 3, 2, 8)
-    counts = sweep.expert_counts(r, 4, 8)
-    assert counts.shape == (4, 3, 8) and counts.sum() == 32 * 3 * 2
-    # the contiguous mapping reproduces layer_loads
-    contiguous = [[list(range(d * 2, d * 2 + 2)) for d in range(4)]] * 3
-    assert np.array_equal(sweep.placed_loads(counts, contiguous), sweep.layer_loads(r, 4, 8, 4))
-    # a replicated expert's pairs split evenly, the lower device taking the extra one
-    c = np.zeros((1, 1, 3), np.int64)
-    c[0, 0] = [5, 2, 4]
-    got = sweep.placed_loads(c, [[[0, 1], [0, 2]]])
-    assert got.tolist() == [[[3 + 2, 2 + 4]]]
-    placements = [sweep.replicated_placement(counts.sum(axis=0)[l], 4, 4, l) for l in range(3)]
-    w = sweep.placed_loads(counts, placements)
-    assert np.array_equal(w.sum(axis=2), counts.sum(axis=2))  # pairs are conserved
+    N, D, E, L = 4, 4, 8, 3
+    counts = sweep.expert_counts(r, N, E)
+    assert counts.shape == (N, L, E) and counts.sum() == 32 * L * 2
+    slots = [sweep.replicated_placement(counts.sum(axis=0)[l], D, D, l) for l in range(L)]
+    copies = [sweep.placement_copies(s, E) for s in slots]
+    placed = np.stack([omodel.placed_device_loads(counts[:, l], copies[l], D) for l in range(L)], axis=1)
+    pl = B.make_placement(copies, D)
+    for pol, opol in (("maxutil", osched.MAXUTIL), ("cumutil", osched.CUMUTIL), ("diffpeak", osched.DIFFPEAK)):
+        got = sweep.run_policy_counts(counts, D, pol, 3, pl)
+        want = [ometrics.step_workload(placed, rs) for rs in osched.run_algorithm1(placed, 3, opol)]
+        assert [g.tolist() for g in got] == [w.tolist() for w in want], pol
+    assert [g.tolist() for g in sweep.run_policy_counts(counts, D, "lockstep", 3, pl)] == \
+        [w.tolist() for w in metrics.lockstep_loads(placed)]
+    assert [g.tolist() for g in sweep.run_policy_counts(counts, D, "separate", 3, pl)] == \
+        [w.tolist() for w in metrics.separate_loads(placed)]
+    contiguous = B.make_placement([[[e // 2] for e in range(E)]] * L, D)
+    w = sweep.layer_loads(r, N, E, D)
+    for pol in ("maxutil", "lockstep"):
+        assert [g.tolist() for g in sweep.run_policy_counts(counts, D, pol, 3, contiguous)] == \
+            [g.tolist() for g in sweep.run_policy(w, pol, 3)]
+        assert [g.tolist() for g in sweep.run_policy_counts(counts, D, pol, 3, None)] == \
+            [g.tolist() for g in sweep.run_policy(w, pol, 3)]
 
 
 def test_report_sections_on_synthetic_routes():
