@@ -25,7 +25,9 @@
  *        pool's expert counts (host-scheduled passes, N * E int32, grown on
  *        demand) and a 256-byte host-mapped status word (device-scheduled
  *        passes); freed when the thread exits;
- *      easybalance_profile_*: a process-wide pool of timing events.
+ *      easybalance_profile_*: a process-wide pool of timing events;
+ *      easybalance_moe_step_noalloc: its static device array
+ *        (EB_NOALLOC_SCRATCH_BYTES per device, allocated by the HIP loader).
  *  - Streams: `stream` is a hipStream_t passed as void* (NULL = null stream).
  *    Device calls only enqueue work on it and never synchronize; the caller
  *    orders calls on one stream or with events.
@@ -260,6 +262,33 @@ int easybalance_moe_step(const eb_model_desc* desc, int32_t n_run, const eb_work
                          const void* const* W_gu, const void* const* W_dn, void* ws,
                          size_t ws_bytes, void* o_out, int32_t* inv_out,
                          const eb_step_views* views, void* stream);
+
+/*
+ * easybalance_moe_step_noalloc -- easybalance_moe_step for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same kernels, same results bit for bit;
+ * the call allocates nothing (no hipMalloc/hipFree, no host heap).  The step's
+ * scratch -- permutation histograms and bases, tile and group lists, work
+ * counters, perm and offsets unless views supplies them, and for long K
+ * (bf16, F >= 8192) the two fp32 partial-sum planes 2 * P * H * 4 bytes --
+ * sits in a static device array of EB_NOALLOC_SCRATCH_BYTES that the library
+ * holds on every device it runs on until the process ends.
+ *
+ * Arguments as for easybalance_moe_step, without ws/ws_bytes; views is
+ * required, with a_perm [P][H] and h [P][F] (dtype, the caller's buffers).
+ * Errors: EB_ERR_INVALID_ARG (as easybalance_moe_step, or views / a_perm / h
+ * NULL), EB_ERR_UNSUPPORTED when the step needs more scratch than the array
+ * holds (the message states the need; e.g. at H = 4096, F = 14336 steps of up
+ * to ~5000 pairs fit), EB_ERR_HIP.
+ * Every call on a device shares that device's array and leaves its contents
+ * behind (nothing in it needs to start at zero: each table is written before
+ * it is read).  Calls that overlap on one device race: order them on one
+ * stream or with events.
+ */
+#define EB_NOALLOC_SCRATCH_BYTES (160u * 1024u * 1024u)
+int easybalance_moe_step_noalloc(const eb_model_desc* desc, int32_t n_run, const eb_work* run,
+                                 const void* const* W_gu, const void* const* W_dn, void* o_out,
+                                 int32_t* inv_out, const eb_step_views* views, void* stream);
 
 /*
  * easybalance_pack_weights -- expert weights into the layout the grouped

@@ -35,7 +35,9 @@ EB_PROFILE_ALL = (1 << EB_NUM_KERNELS) - 1
 EXPORTS = ["easybalance_version", "easybalance_last_error", "easybalance_route",
            "easybalance_schedule", "easybalance_moe_step_workspace_size", "easybalance_moe_step",
            "easybalance_combine", "easybalance_profile_begin", "easybalance_profile_end",
-           "easybalance_pass_state_size", "easybalance_run_pass", "easybalance_pack_weights"]
+           "easybalance_pass_state_size", "easybalance_run_pass", "easybalance_pack_weights",
+           "easybalance_moe_step_noalloc"]
+EB_NOALLOC_SCRATCH_BYTES = 160 * 1024 * 1024
 
 
 class eb_model_desc(ctypes.Structure):
@@ -114,6 +116,8 @@ def lib() -> ctypes.CDLL:
     l.easybalance_moe_step.restype = ctypes.c_int
     l.easybalance_moe_step.argtypes = [D, I32, W, P, P, P, ctypes.c_size_t, P, P,
                                        ctypes.POINTER(eb_step_views), P]
+    l.easybalance_moe_step_noalloc.restype = ctypes.c_int
+    l.easybalance_moe_step_noalloc.argtypes = [D, I32, W, P, P, P, P, ctypes.POINTER(eb_step_views), P]
     l.easybalance_combine.restype = ctypes.c_int
     l.easybalance_combine.argtypes = [D, I32, W, P, P, P, P]
     l.easybalance_pass_state_size.restype = ctypes.c_int
@@ -224,6 +228,18 @@ def easybalance_moe_step(desc, run, n_run, W_gu, W_dn, ws, ws_bytes, o_out, inv_
     _check("easybalance_moe_step", lib().easybalance_moe_step(
         ctypes.byref(desc), n_run, run, gu, dn, _ptr(ws), ws_bytes, _ptr(o_out), _ptr(inv_out),
         v, stream))
+
+
+def easybalance_moe_step_noalloc(desc, run, n_run, W_gu, W_dn, o_out, inv_out, views,
+                                 stream=None) -> None:
+    """views: dict with at least "a_perm" and "h" (the caller's buffers)."""
+    gu, dn = _ptr_array(W_gu), _ptr_array(W_dn)
+    v = None
+    if views is not None:
+        v = ctypes.byref(eb_step_views(_ptr(views.get("a_perm")), _ptr(views.get("h")),
+                                       _ptr(views.get("perm")), _ptr(views.get("offsets"))))
+    _check("easybalance_moe_step_noalloc", lib().easybalance_moe_step_noalloc(
+        ctypes.byref(desc), n_run, run, gu, dn, _ptr(o_out), _ptr(inv_out), v, stream))
 
 
 def easybalance_pack_weights(desc, kind, n, src, dst, stream=None) -> None:

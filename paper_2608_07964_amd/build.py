@@ -26,7 +26,7 @@ SYNTH_HOST_SRC = os.path.join(ROOT, "synth", "gen_host.c")
 SYNTH_HOST_LIB = os.path.join(ROOT, "synth", "libsynthhost.so")
 
 SOURCES = ["api.cpp", "schedule.cpp", "pass.cpp", "route.hip", "permute.hip", "gemm.hip", "combine.hip",
-           "sched_dev.hip"]
+           "sched_dev.hip", "noalloc.hip"]
 
 ARCH = os.environ.get("EB_OFFLOAD_ARCH", "gfx950")
 HIPCC = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
