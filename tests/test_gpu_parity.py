@@ -372,3 +372,32 @@ def test_route_nan_logits_pick_distinct_experts(name, device):
     assert np.array_equal(idx2, idx) and np.array_equal(counts2, counts)
     assert np.array_equal(np.isnan(w), np.isnan(w2)) and np.array_equal(w[~np.isnan(w)], w2[~np.isnan(w2)])
     assert np.isnan(w[5]).all()
+
+
+def test_route_stage_one_workgroup_per_token_bf16(device):
+    """bf16 stacks with E <= 8 and H > 4096 route one token per workgroup
+    (the LDS-staged wavefront router holds H <= 4096): the same parity as
+    test_route_stage on that path, ragged token counts included."""
+    B = _binding()
+    cfg = mini(BY_NAME["mixtral_bf16"], H=8192, F=256, T=70, L=1)
+    log(f"route parity {cfg.name} H={cfg.H}")
+    inp = DeviceInputs(cfg, device, weights=False)
+    P = host_weights(cfg)
+    desc = B.make_desc(cfg.L, cfg.H, cfg.F, cfg.E, cfg.k, cfg.S, cfg.D, cfg.dtype, cfg.eps)
+    for T in (cfg.T, 1, 33):
+        x = inp.x0[0, :T].clone()
+        a = torch.empty(T, cfg.H, dtype=torch.bfloat16, device=device)
+        z = torch.empty(T, cfg.E, dtype=torch.float32, device=device)
+        idx = torch.empty(T, cfg.k, dtype=torch.int32, device=device)
+        w = torch.empty(T, cfg.k, dtype=torch.float32, device=device)
+        counts = torch.empty(cfg.E, dtype=torch.int32, device=device)
+        B.easybalance_route(desc, 0, T, x, inp.g[0], inp.Wg[0], inp.bias[0], a, z, idx, w, counts)
+        torch.cuda.synchronize()
+        a_ref = omodel.rmsnorm_cast(to_np(x), P.gain(0), cfg.eps, cast_fn(cfg.dtype))
+        assert_close(to_np(a), a_ref, cfg.dtype, "a")
+        zg = to_np(z)
+        assert_close(zg, omodel.router_logits(to_np(a), P.router(0), P.bias(0)), cfg.dtype, "logits")
+        idx_np = idx.cpu().numpy()
+        assert np.array_equal(idx_np, omodel.topk_indices(zg, cfg.k))
+        assert np.array_equal(counts.cpu().numpy(), omodel.expert_counts(idx_np, cfg.E))
+        assert_close(to_np(w), omodel.gate_weights(zg, idx_np), cfg.dtype, "w")
