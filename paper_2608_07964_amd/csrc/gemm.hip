@@ -515,10 +515,13 @@ __device__ __forceinline__ void run_item(const GroupedProblem& p, bf16_t* smem, 
 
 // Persistent grouped GEMM.  Work item = (group, n-tile, m-tile); a group of
 // R rows has ceil(R / 256) m-tiles sharing its rows evenly, enumerated group
-// by group, n-tile-major, m-tile fastest, so consecutive items share the
-// weight tile and, running at the same pace, read each weight stage from L2
-// once (unequal m-tiles drift apart and fetch the weights again: 2.2-3.5x
-// the weight bytes for two to three m-tiles).  Workgroup b runs on XCD b % 8 (round-robin
+// by group, then by blocks of kMBlock m-tiles, n-tile-major inside a block,
+// m-tile fastest, so consecutive items share the weight tile and, running at
+// the same pace, read each weight stage from L2 once (unequal m-tiles drift
+// apart and fetch the weights again: 2.2-3.5x the weight bytes for two to
+// three m-tiles).  The blocks bound how often a large group's activation rows
+// are streamed: once per window of n-tiles rather than once per n-tile (with
+// tens of m-tiles, 28 times over for a 7168-wide down projection).  Workgroup b runs on XCD b % 8 (round-robin
 // dispatch) and takes items from its XCD's contiguous eighth of the list
 // through that XCD's atomic counter, so items running together on one L2
 // share weight and activation tiles and no workgroup idles while its XCD has
@@ -528,6 +531,11 @@ __device__ __forceinline__ void run_item(const GroupedProblem& p, bf16_t* smem, 
 // current one and its result used at its end.  Each item runs in the tile
 // shape of the rows it holds; all shapes accumulate K in the same order, so a
 // row's result does not depend on the shape or on which workgroup ran it.
+// m-tiles per block of the item order (see grouped_gemm_bf16): a window of
+// the 32 items one XCD runs at a time then spans 4 m-tiles x 8 n-tiles, so
+// it streams 4 activation and 8 weight tiles instead of 32 and 1.
+constexpr int kMBlock = 4;
+
 template <int MODE>
 __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_bf16(GroupedProblem p, WeightTable wt,
                                                                  const bf16_t* __restrict__ A,
@@ -572,11 +580,15 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_bf16(GroupedProblem 
     // cover its m-tiles it .. it + mt - 1, so item / nsub is one of them
     const int4 gd = p.tiles[it / nsub];  // key, first row, rows, first m-tile
     const int mt = (gd.z + BM - 1) / BM;
-    // within the group: K part slowest, then n-tile, m-tile fastest
+    // within the group: K part slowest, then blocks of kMBlock m-tiles, then
+    // n-tile, m-tile fastest (the last block holds the mt % kMBlock rest)
     const int local = it - gd.w * nsub;
     const int kh = local / (mt * n_ntiles);
     const int rem = local - kh * mt * n_ntiles;
-    const int ni = rem / mt, mi = rem - ni * mt;
+    const int mb = rem / (kMBlock * n_ntiles);
+    const int gm = min(kMBlock, mt - mb * kMBlock);
+    const int rb = rem - mb * kMBlock * n_ntiles;
+    const int ni = rb / gm, mi = mb * kMBlock + (rb - ni * gm);
     const int nks = K / BK / ksplit, ks0 = kh * nks;
     float* part = ksplit > 1 ? p.partial + (size_t)kh * p.P * p.H : nullptr;
     // the group's mt m-tiles share its rows evenly (whole 32-row blocks), so
