@@ -16,7 +16,7 @@ from oracle import model as omodel
 from oracle import permute as operm
 from oracle import sched as osched
 from oracle.numerics import cast_fn
-from synth import BY_NAME, CONFIGS, gen, mini
+from synth import BY_NAME, CONFIGS, Config, gen, mini
 from synth.device import DeviceInputs, fill_
 
 from gpu_helpers import assert_close, ensure_packed, host_weights, log, make_stack, to_np
@@ -32,6 +32,25 @@ LONGK = mini(BY_NAME["mixtral_bf16"], H=256, F=8192, T=96, L=2)
 ROWONCE = mini(BY_NAME["dsv3_share_bf16"], H=2048, T=96, L=2)
 STEP_CFGS = MINIS + [LONGK, ROWONCE]
 STEP_IDS = IDS + [LONGK.name + "_longk", ROWONCE.name + "_rowonce"]
+# the ABI's shape limits and the method's degenerate mixtures:
+# * k + S = 16 expert slots per token (12 routed picks of 64, 4 shared), also
+#   with rows long enough for the read-once grouping;
+# * k = E (every token on every expert), bf16 and fp32;
+# * L * (E + S) = 15360 keys in one step's grouping, with E = 252 experts
+#   (not a multiple of the router's 32-expert blocks)
+MAXSLOTS = Config("maxslots_bf16", L=2, H=256, F=256, E=64, k=12, S=4, D=8, N=4, T=96, dtype="bf16",
+                  skew="zipf", skew_param=1.1, seed=20261001)
+LIMIT_CFGS = [
+    MAXSLOTS,
+    MAXSLOTS.scaled(name="maxslots_rowonce_bf16", H=2048, T=64, seed=20261002),
+    Config("dense_bf16", L=2, H=256, F=256, E=8, k=8, S=0, D=4, N=4, T=96, dtype="bf16",
+           skew="zipf", skew_param=1.0, seed=20261003),
+    Config("dense_f32", L=2, H=256, F=128, E=8, k=8, S=1, D=8, N=3, T=70, dtype="f32",
+           skew="dirichlet", skew_param=0.3, seed=20261004),
+    Config("maxkeys_bf16", L=60, H=256, F=128, E=252, k=2, S=4, D=4, N=4, T=48, dtype="bf16",
+           skew="zipf", skew_param=1.2, seed=20261005),
+]
+LIMIT_IDS = [c.name for c in LIMIT_CFGS]
 
 
 def _binding():
@@ -101,7 +120,7 @@ def test_device_generator_bit_exact(device):
             assert np.array_equal(t.cpu().numpy(), ref)
 
 
-@pytest.mark.parametrize("cfg", MINIS, ids=IDS)
+@pytest.mark.parametrize("cfg", MINIS + LIMIT_CFGS, ids=IDS + LIMIT_IDS)
 def test_route_stage(cfg, device):
     B = _binding()
     log(f"route parity {cfg.name}")
@@ -142,7 +161,7 @@ def _route_entry(B, desc, cfg, inp, j, l, T, device):
     return bufs
 
 
-@pytest.mark.parametrize("cfg", STEP_CFGS, ids=STEP_IDS)
+@pytest.mark.parametrize("cfg", STEP_CFGS + LIMIT_CFGS, ids=STEP_IDS + LIMIT_IDS)
 def test_moe_step_and_combine_stage(cfg, device):
     """One cross-layer step with entries at different layers, ragged and empty
     token counts; every stage checked against the oracle on the GPU's inputs."""
