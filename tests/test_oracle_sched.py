@@ -2,6 +2,7 @@
 CumUtil / DiffPeak of Section 5.2, Eqs. 2-3): hand-worked examples, an
 independent brute force over subsets with exact fractions, and the invariants
 the paper states (losslessness, per-micro-batch order, worst-case safety)."""
+import functools
 import itertools
 import json
 import os
@@ -154,3 +155,67 @@ def test_maxutil_never_worse_than_separate():
         eb = sched.run_algorithm1(loads, max(1, int(0.75 * N)), sched.MAXUTIL)
         sep = sched.separate_steps(N, L)
         assert metrics.utilization(loads, eb) >= metrics.utilization(loads, sep)
+
+
+def _offline_optimum(loads: np.ndarray, m: int) -> int:
+    """Smallest summed per-step peak load (sum over steps of max_d W_i,d) over
+    every schedule Algorithm 1 may run: at each step any set of at least
+    min(m, |pool|) micro-batches still in the pool advances one layer.  An
+    exhaustive search over the micro-batches' layer positions, written
+    independently of oracle.sched."""
+    N, L, _ = loads.shape
+
+    @functools.lru_cache(maxsize=None)
+    def best(state):
+        pool = [j for j in range(N) if state[j] < L]
+        if not pool:
+            return 0
+        cost = None
+        for r in range(min(m, len(pool)), len(pool) + 1):
+            for R in itertools.combinations(pool, r):
+                peak = int(sum(loads[j, state[j]] for j in R).max())
+                nxt = tuple(s + (j in R) for j, s in enumerate(state))
+                c = peak + best(nxt)
+                cost = c if cost is None else min(cost, c)
+        return cost
+
+    return best((0,) * N)
+
+
+def test_offline_optimum_hand_worked():
+    # one layer, two devices: complementary loads merge (peak 4 < 3 + 3),
+    # identical ones gain nothing (6 either way)
+    assert _offline_optimum(np.array([[[3, 1]], [[1, 3]]]), 1) == 4
+    assert _offline_optimum(np.array([[[3, 1]], [[3, 1]]]), 1) == 6
+    # m = 2 forces both together at every step: the lock-step sum of peaks
+    loads = np.array([[[3, 1], [0, 2]], [[1, 3], [2, 2]]])
+    assert _offline_optimum(loads, 2) == 4 + 4
+
+
+def test_greedy_against_offline_optimum():
+    """Every policy's schedule is one the search considers, so the optimum is
+    never larger; it is also bounded below by the total work over D, and
+    above by lock-step (and, for m = 1, by separate steps).  The greedy /
+    optimum ratio is reported, not gated."""
+    rng = np.random.default_rng(2026_12_02)
+    ratios = {p: [] for p in (sched.MAXUTIL, sched.CUMUTIL, sched.DIFFPEAK)}
+    for _ in range(400):
+        N, L, D = int(rng.integers(1, 4)), int(rng.integers(1, 4)), int(rng.integers(1, 5))
+        m = int(rng.integers(1, N + 1))
+        loads = rng.integers(0, 6, size=(N, L, D)).astype(np.int64)
+        opt = _offline_optimum(loads, m)
+        total = int(loads.sum())
+        peaks = lambda steps: sum(int(metrics.step_workload(loads, s).max()) for s in steps)
+        assert opt * D >= total
+        assert opt <= peaks(sched.lockstep_steps(N, L))
+        if m == 1:
+            assert opt <= peaks(sched.separate_steps(N, L))
+        if D == 1:
+            assert opt == total
+        for p in ratios:
+            g = peaks(sched.run_algorithm1(loads, m, p))
+            assert g >= opt
+            ratios[p].append(Fraction(g, opt) if opt else Fraction(1))
+    for p, r in ratios.items():
+        print(f"policy {p}: greedy / optimum mean {float(sum(r) / len(r)):.4f}, max {float(max(r)):.3f}, "
+              f"optimal in {sum(x == 1 for x in r)}/{len(r)}")
