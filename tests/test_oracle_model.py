@@ -141,6 +141,33 @@ def test_moe_layer_single_expert_is_dense_ffn():
             assert out.x_out[t, n] == pytest.approx(x[t, n] + cd[n] * hv[pd[n]], rel=1e-12)
 
 
+def test_moe_layer_every_expert_is_the_dense_softmax_mixture():
+    """k = E: top-k keeps every expert, so the layer is x + sum_e p_e FFN_e(a)
+    with p the softmax of all E logits -- a dense mixture, written here with
+    scalar loops and the closed-form selection-matrix experts."""
+    rng = np.random.default_rng(11)
+    H, F, T, E = 5, 7, 3, 4
+    experts = [tuple(_selection(r, c, rng) for r, c in ((F, H), (F, H), (H, F))) for _ in range(E)]
+    Wr = rng.normal(size=(E, H))
+    b = rng.normal(size=E)
+    P = model.Weights(gain=lambda l: np.ones(H), router=lambda l: Wr, bias=lambda l: b,
+                      gate_up=lambda l, e: (experts[e][0][0], experts[e][1][0]),
+                      down=lambda l, e: experts[e][2][0])
+    x = rng.normal(size=(T, H))
+    out = model.moe_layer(x, 0, P, E=E, k=E, S=0, eps=1e-6, dtype="f32")
+    for t in range(T):
+        a = x[t] / math.sqrt(np.mean(x[t] ** 2) + 1e-6)
+        z = [sum(a[i] * Wr[e, i] for i in range(H)) + b[e] for e in range(E)]
+        den = sum(math.exp(v) for v in z)
+        for n in range(H):
+            want = x[t, n]
+            for e in range(E):
+                (_, pg, cg), (_, pu, cu), (_, pd, cd) = experts[e]
+                f = pd[n]
+                want += math.exp(z[e]) / den * cd[n] * _silu_scalar(cg[f] * a[pg[f]]) * cu[f] * a[pu[f]]
+            assert out.x_out[t, n] == pytest.approx(want, rel=1e-10, abs=1e-12)
+
+
 def test_moe_layer_invariants():
     rng = np.random.default_rng(8)
     L, H, F, E, S, k, T = 1, 16, 12, 6, 2, 2, 10
