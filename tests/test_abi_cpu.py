@@ -274,3 +274,33 @@ def test_placement_argument_checks():
         B.easybalance_schedule(ids, counts, E, D, 1, layers=[0, 2], placement=pl)
     with pytest.raises(B.EasyBalanceError):          # made for another E
         B.easybalance_schedule(ids, np.ones((2, 6), np.int32), 6, D, 1, layers=[0, 1], placement=pl)
+
+
+@pytest.mark.parametrize("name", ["mixtral_bf16", "qwen_moe_bf16", "dsv2_lite_bf16", "dsv3_share_bf16"])
+def test_scheduler_cost_native_against_oracle(name):
+    """Context for the paper's Table 3 (scheduling time per step): one
+    Schedule decision over a full pool of the stack's N micro-batches at its
+    D and m, by the native host scheduler (through the binding) and by the
+    oracle's plain-Python one, on the same random counts; the run sets agree
+    and the per-decision times are printed (reported, not gated)."""
+    import time
+    from synth import BY_NAME
+    cfg = BY_NAME[name]
+    rng = np.random.default_rng(17)
+    ids = list(range(cfg.N))
+    trials = [rng.integers(0, 200, size=(cfg.N, cfg.E)).astype(np.int32) for _ in range(5)]
+    B.easybalance_schedule(ids, trials[0], cfg.E, cfg.D, cfg.m, B.EB_POLICY_DIFFPEAK)  # loads the library
+    for policy in (osched.MAXUTIL, osched.CUMUTIL, osched.DIFFPEAK):
+        t_nat = t_py = 0.0
+        for counts in trials:
+            t0 = time.perf_counter()
+            mask, _ = B.easybalance_schedule(ids, counts, cfg.E, cfg.D, cfg.m, POL[policy])
+            t1 = time.perf_counter()
+            loads = {j: omodel.device_loads(counts[j], cfg.D) for j in ids}
+            want = osched.schedule(ids, loads, cfg.D, cfg.m, policy)
+            t2 = time.perf_counter()
+            assert tuple(j for j in ids if (mask >> j) & 1) == want
+            t_nat += t1 - t0
+            t_py += t2 - t1
+        print(f"{name} N={cfg.N} D={cfg.D} m={cfg.m} policy {policy}: native {1e6 * t_nat / len(trials):.0f} us, "
+              f"oracle (plain Python) {1e3 * t_py / len(trials):.2f} ms per decision")
