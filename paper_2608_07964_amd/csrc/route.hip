@@ -4,9 +4,12 @@
 //                        z = a Wg^T + bias and the top-k with its softmax
 //                        weights
 //   rmsnorm_kernel +     other bf16 stacks: RMSNorm, then the router GEMM on
-//   route_mfma_kernel    the matrix cores (split-K over the 4 wavefronts) and
-//                        the top-k of the workgroup's 32 tokens from an LDS
-//                        logit tile
+//   route_mfma_kernel /  the matrix cores and the top-k of the workgroup's 32
+//   route_lds_kernel     tokens from an LDS logit tile (E <= 64: 32 tokens,
+//                        split-K over the 4 wavefronts, operands straight into
+//                        registers; E > 64: 128 tokens, 8 wavefronts splitting
+//                        tokens and experts, operands staged through LDS as
+//                        whole cache lines)
 //   rmsnorm_kernel +     other fp32 stacks: RMSNorm, an LDS-tiled fp32
 //   logits_kernel +      VALU GEMM for z, then the top-k
 //   topk_kernel
@@ -474,7 +477,7 @@ __global__ __launch_bounds__(256) void route_token_kernel(RBA rba, int H, int E,
 }
 
 // ---------------------------------------------------------------------------
-// Router logits on the matrix cores and top-k (bf16 stacks, E <= 256).
+// Router logits on the matrix cores and top-k (bf16 stacks, E <= 64).
 // A workgroup takes 32 tokens and all experts (padded to NB blocks of 32);
 // its 4 wavefronts split K into quarters, each accumulating a 32 x 32 NB
 // partial with v_mfma_f32_32x32x16_bf16 from operands loaded straight from L2
@@ -586,6 +589,170 @@ __global__ __launch_bounds__(256) void route_mfma_kernel(RBA rba, int H, int E, 
 }
 
 // ---------------------------------------------------------------------------
+// Router logits for E > 64 experts (bf16): 128 tokens per workgroup of 8
+// wavefronts, wavefront w taking tokens 64 (w / 4) .. + 63 and the NBW
+// 32-expert blocks from NBW (w % 4) on, every wavefront over the whole of K.
+// Workgroups take the batch's 128-token tiles in order (entry by entry, from
+// the batch's 32-token block table), so consecutive tiles run on different
+// XCDs.  K advances 64 columns at a time through an
+// LDS ring of kRouteStages stages filled by buffer loads straight into LDS:
+// 1 KB per load is 8 rows x 128 bytes, whole cache lines, and each row's
+// 16-byte chunk c sits at c ^ ((row >> 1) & 7) so the fragment reads are
+// conflict-free.  Every logit is one chain of MFMAs over K in ascending order
+// plus the bias, so it does not depend on the token's block or batch.  The
+// logit tile for the top-k reuses the ring once the K loop is done.
+constexpr int kRouteStages = 3;
+constexpr int kRouteTokens = 128;
+
+template <int NBW, class RBA>
+__global__ __launch_bounds__(512) void route_lds_kernel(RBA rba, int H, int E, int k, int norm_topk) {
+  constexpr int NB = 4 * NBW;                       // 32-expert blocks of the workgroup
+  constexpr int A_ELEMS = kRouteTokens * 64;        // one stage of the token rows (16 KB)
+  constexpr int B_ELEMS = NB * 32 * 64;             // one stage of the router rows
+  constexpr int RING = kRouteStages * (A_ELEMS + B_ELEMS);
+  constexpr int ZS = NB * 32 + 1;                   // padded row of the logit tile (floats)
+  static_assert(kRouteTokens * ZS * 4 <= RING * 2, "logit tile fits in the ring");
+  __shared__ __attribute__((aligned(1024))) bf16_t ring[RING];
+  // the ring is written by global->LDS loads the compiler does not see
+  asm volatile("" ::"v"(ring) : "memory");
+  const RouteBatch& rb = rba.get();
+  // workgroup q: the q-th 128-token tile of the batch, entries in order
+  // (an entry of b 32-token blocks has ceil(b / 4) tiles)
+  int ei = -1, t0 = 0;
+  for (int i = 0, base = 0; i < rb.n; ++i) {
+    const int nt = (rb.blk0[i + 1] - rb.blk0[i] + 3) / 4;
+    if ((int)blockIdx.x < base + nt) {
+      ei = i;
+      t0 = ((int)blockIdx.x - base) * kRouteTokens;
+      break;
+    }
+    base += nt;
+  }
+  if (ei < 0) return;  // past the live tiles
+  const int T = rb.tok0[ei + 1] - rb.tok0[ei];
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave >> 2, wn = wave & 3;
+  const int lrow = lane & 31, khalf = lane >> 5;
+  const bf16_t* __restrict__ a = static_cast<const bf16_t*>(rb.e[ei].a);
+  const bf16_t* __restrict__ Wg = static_cast<const bf16_t*>(rb.e[ei].Wg);
+  const float* __restrict__ bias = rb.e[ei].bias;
+  float* __restrict__ z = rb.e[ei].z;
+  int32_t* __restrict__ idx = rb.e[ei].idx;
+  float* __restrict__ w = rb.e[ei].w;
+  // buffer descriptors: rows past the tokens' or the experts' end read zeros
+  const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<bf16_t*>(a + (size_t)t0 * H), (short)0, min(T - t0, kRouteTokens) * H * 2, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<bf16_t*>(Wg), (short)0, (int)(E * H * 2), 0x00020000);
+  // load lane l: row l / 8 of an 8-row block, physical chunk l % 8 holding
+  // logical chunk (l % 8) ^ ((row >> 1) & 7); a block starting at a multiple
+  // of 16 rows gives ((l / 8) >> 1) & 7, one starting 8 rows later flips bit 2
+  const int lr = lane >> 3, lp = lane & 7;
+  const int c_even = lp ^ ((lr >> 1) & 7), c_odd = c_even ^ 4;
+  const int row_b = 2 * H;                // bytes of one row
+  const int voff_even = lr * row_b + c_even * 16, voff_odd = lr * row_b + c_odd * 16;
+  // wave w loads token rows 16 w + 8 j (j < 2) and router rows 4 NB w + 8 j
+  // (j < NB / 2); block parity j & 1 in both
+  constexpr int kALoads = kRouteTokens / 8 / 8, kBLoads = NB * 32 / 8 / 8;
+  const int nst = H / 64;
+  auto issue = [&](int st, int slot) {
+    st = min(st, nst - 1);  // past the last stage: reload it into a slot nobody reads
+    bf16_t* sa = ring + slot * (A_ELEMS + B_ELEMS);
+    bf16_t* sb = sa + A_ELEMS;
+#pragma unroll
+    for (int j = 0; j < kALoads; ++j) {
+      const int r0 = kALoads * 8 * wave + 8 * j;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, sa + r0 * 64, 16, (j & 1) ? voff_odd : voff_even,
+                                               r0 * row_b + st * 128, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < kBLoads; ++j) {
+      const int r0 = kBLoads * 8 * wave + 8 * j;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, sb + r0 * 64, 16, (j & 1) ? voff_odd : voff_even,
+                                               r0 * row_b + st * 128, 0, 0);
+    }
+  };
+  constexpr int kLoadsPerStage = kALoads + kBLoads;  // this wavefront's loads of one stage
+  constexpr int kWaitAhead = kLoadsPerStage * (kRouteStages - 2);
+  static_assert(kWaitAhead < 64, "vmcnt range");
+  floatx16_t acc[2][NBW];
+#pragma unroll
+  for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[mb][nb][v] = 0.f;
+  const int sw = (lrow >> 1) & 7;
+#pragma unroll
+  for (int s = 0; s < kRouteStages - 1; ++s) issue(s, s);
+  for (int s = 0; s < nst; ++s) {
+    // stage s has landed once only the later stages' loads are in flight, and
+    // this wave's fragment reads of stage s-1 are done (lgkmcnt 0) before the
+    // barrier lets another wave refill that slot
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt((kWaitAhead & 15) | ((kWaitAhead >> 4) << 14) | (7 << 4));
+    __builtin_amdgcn_s_barrier();  // every wave's part of stage s is in LDS; stage s-1 is read
+    asm volatile("" ::: "memory");
+    const int slot = s % kRouteStages;
+    issue(s + kRouteStages - 1, (s + kRouteStages - 1) % kRouteStages);
+    const bf16_t* sa = ring + slot * (A_ELEMS + B_ELEMS) + (64 * wm) * 64;
+    const bf16_t* sb = ring + slot * (A_ELEMS + B_ELEMS) + A_ELEMS + (32 * NBW * wn) * 64;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const int ch = ((2 * ks + khalf) ^ sw) * 8;
+      bf16x8_t af[2], bfr[NBW];
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb) af[mb] = *reinterpret_cast<const bf16x8_t*>(sa + (mb * 32 + lrow) * 64 + ch);
+#pragma unroll
+      for (int nb = 0; nb < NBW; ++nb) bfr[nb] = *reinterpret_cast<const bf16x8_t*>(sb + (nb * 32 + lrow) * 64 + ch);
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb)
+          acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mb], bfr[nb], acc[mb][nb], 0, 0, 0);
+    }
+  }
+  // every load (including those past the last stage) has landed and every
+  // wave is done reading the ring before the logit tile overwrites it
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(7 << 4);
+  __syncthreads();
+  float* zs = reinterpret_cast<float*>(ring);
+  // acc[mb][nb][v]: expert 32 (NBW wn + nb) + lane % 32, token
+  // 64 wm + 32 mb + 8 (v / 4) + 4 (lane / 32) + v % 4
+#pragma unroll
+  for (int mb = 0; mb < 2; ++mb) {
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb) {
+      const int e = 32 * (NBW * wn + nb) + lrow;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int tl = 64 * wm + 32 * mb + 8 * (v >> 2) + 4 * khalf + (v & 3);
+        if (e < E) {
+          const float ze = acc[mb][nb][v] + bias[e];
+          zs[tl * ZS + e] = ze;
+          if (z != nullptr && t0 + tl < T) z[(size_t)(t0 + tl) * E + e] = ze;
+        }
+      }
+    }
+  }
+  __syncthreads();
+  // 8 lanes per token, two tokens per group of 8 lanes
+#pragma unroll
+  for (int half = 0; half < 2; ++half) {
+    const int tl = (threadIdx.x >> 3) + 64 * half, t = t0 + tl;
+    if (t < T) {
+      if (k <= 8)
+        topk_group8<NB * 4, 8>(threadIdx.x & 7, E, k, norm_topk, zs + tl * ZS, idx + (size_t)t * k,
+                               w + (size_t)t * k);
+      else
+        topk_group8<NB * 4, 16>(threadIdx.x & 7, E, k, norm_topk, zs + tl * ZS, idx + (size_t)t * k,
+                                w + (size_t)t * k);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Top-k from logits in global memory (fp32 stacks without the fused path),
 // one thread per token.
 __global__ __launch_bounds__(256) void topk_kernel(int T, int E, int k, int norm_topk,
@@ -630,13 +797,17 @@ hipError_t route_batch_typed(const eb_model_desc& d, RBA rba, const RouteBatch* 
       prof_start(EB_K_ROUTE_LOGITS, s);
       if (sizeof(TA) == 2) {
         const dim3 grid(grid_blocks);
+        // 128-token tiles: at most a quarter of the blocks plus one per entry
+        const dim3 grid_tiles((grid_blocks + 3) / 4 + grid_entries);
         const int nb = (d.E + 31) / 32;
         if (nb <= 2)
           hipLaunchKernelGGL((route_mfma_kernel<2, RBA>), grid, dim3(256), 0, s, rba, d.H, d.E, d.k, d.norm_topk);
         else if (nb <= 4)
-          hipLaunchKernelGGL((route_mfma_kernel<4, RBA>), grid, dim3(256), 0, s, rba, d.H, d.E, d.k, d.norm_topk);
+          hipLaunchKernelGGL((route_lds_kernel<1, RBA>), grid_tiles, dim3(512), 0, s, rba, d.H, d.E, d.k,
+                             d.norm_topk);
         else
-          hipLaunchKernelGGL((route_mfma_kernel<8, RBA>), grid, dim3(256), 0, s, rba, d.H, d.E, d.k, d.norm_topk);
+          hipLaunchKernelGGL((route_lds_kernel<2, RBA>), grid_tiles, dim3(512), 0, s, rba, d.H, d.E, d.k,
+                             d.norm_topk);
         prof_stop(EB_K_ROUTE_LOGITS, s);
       } else {
         if (host_rb == nullptr) return hipErrorInvalidValue;
