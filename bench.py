@@ -123,8 +123,8 @@ def main() -> int:
                          "of known size for calibrating rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU "
-              "expert-parallel path is not part of this build", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); an expert-parallel "
+              "run over several GPUs is not implemented", file=sys.stderr)
         return 2
 
     import numpy as np
