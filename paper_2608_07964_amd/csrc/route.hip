@@ -388,9 +388,12 @@ template <> struct Vec8<float> {
 constexpr int kTokChunks = 4;  // 8-element chunks per thread: H <= 256 * 8 * 4
 constexpr int kTokMaxH = 256 * 8 * kTokChunks;
 
-template <typename TA, int EMAX, class RBA>
-__global__ __launch_bounds__(256) void route_token_kernel(RBA rba, int H, int E, int k,
-                                                          int norm_topk, float eps) {
+// KC: 8-element chunks per thread (H <= 256 * 8 * KC).  The 2-chunk form for
+// H <= 4096 fits 64 registers, so a CU holds 8 of these workgroups (a
+// 2048-token launch in one round).
+template <typename TA, int EMAX, int KC, class RBA>
+__global__ __launch_bounds__(256, KC == 2 ? 8 : 1) void route_token_kernel(RBA rba, int H, int E, int k,
+                                                                           int norm_topk, float eps) {
   __shared__ float red[4];
   __shared__ float red_z[4][EMAX + 1];
   const RouteBatch& rb = rba.get();
@@ -409,10 +412,10 @@ __global__ __launch_bounds__(256) void route_token_kernel(RBA rba, int H, int E,
   const float* xr = x + (size_t)t * H;
   const int nchunk = H >> 3;
   // thread tid owns chunks c = tid + 256 i (8 elements each), kept in registers
-  float xs[kTokChunks][8];
+  float xs[KC][8];
   float ss = 0.f;
 #pragma unroll
-  for (int i = 0; i < kTokChunks; ++i) {
+  for (int i = 0; i < KC; ++i) {
     const int c = tid + 256 * i;
     if (c < nchunk) {
       const float4 u = reinterpret_cast<const float4*>(xr + 8 * c)[0];
@@ -422,7 +425,7 @@ __global__ __launch_bounds__(256) void route_token_kernel(RBA rba, int H, int E,
     }
   }
 #pragma unroll
-  for (int i = 0; i < kTokChunks; ++i)
+  for (int i = 0; i < KC; ++i)
     if (tid + 256 * i < nchunk)
 #pragma unroll
       for (int q = 0; q < 8; ++q) ss = fmaf(xs[i][q], xs[i][q], ss);
@@ -435,7 +438,7 @@ __global__ __launch_bounds__(256) void route_token_kernel(RBA rba, int H, int E,
   for (int e = 0; e < EMAX; ++e) acc[e] = 0.f;
   TA* ar = a + (size_t)t * H;
 #pragma unroll
-  for (int i = 0; i < kTokChunks; ++i) {
+  for (int i = 0; i < KC; ++i) {
     const int c = tid + 256 * i;
     if (c < nchunk) {
       const int h = 8 * c;
@@ -782,12 +785,15 @@ hipError_t route_batch_typed(const eb_model_desc& d, RBA rba, const RouteBatch* 
   if (grid_tokens > 0) {
     if (fused_token_path<TA>(d)) {
       prof_start(EB_K_ROUTE_LOGITS, s);
-      if (d.E <= 8)
-        hipLaunchKernelGGL((route_token_kernel<TA, 8, RBA>), dim3(grid_tokens), dim3(256), 0, s, rba, d.H,
+      if (d.E <= 8 && d.H <= 256 * 8 * 2)
+        hipLaunchKernelGGL((route_token_kernel<TA, 8, 2, RBA>), dim3(grid_tokens), dim3(256), 0, s, rba, d.H,
                            d.E, d.k, d.norm_topk, d.rms_eps);
+      else if (d.E <= 8)
+        hipLaunchKernelGGL((route_token_kernel<TA, 8, kTokChunks, RBA>), dim3(grid_tokens), dim3(256), 0, s,
+                           rba, d.H, d.E, d.k, d.norm_topk, d.rms_eps);
       else
-        hipLaunchKernelGGL((route_token_kernel<TA, 64, RBA>), dim3(grid_tokens), dim3(256), 0, s, rba, d.H,
-                           d.E, d.k, d.norm_topk, d.rms_eps);
+        hipLaunchKernelGGL((route_token_kernel<TA, 64, kTokChunks, RBA>), dim3(grid_tokens), dim3(256), 0, s,
+                           rba, d.H, d.E, d.k, d.norm_topk, d.rms_eps);
       prof_stop(EB_K_ROUTE_LOGITS, s);
     } else {
       prof_start(EB_K_ROUTE_NORM, s);
