@@ -247,9 +247,10 @@ int enqueue_step_dev(const eb_model_desc& d, int N, int T, const RunTable* rt, c
   const bool fuse = w.partial != nullptr;
   if ((rc = run_gemms(d, sh, w, wt, o, s, !fuse))) return rc;
   if (fuse)
-    return hip_status(launch_combine_split_dev(rt, (int)sh.tokens, w.partial, (long long)sh.P * d.H, inv, s),
-                      "combine");
-  return hip_status(launch_combine_dev(rt, (int)sh.tokens, d.dtype, o, inv, s), "combine");
+    return hip_status(
+        launch_combine_split_dev(rt, d.k + d.S, (int)sh.tokens, w.partial, (long long)sh.P * d.H, inv, s),
+        "combine");
+  return hip_status(launch_combine_dev(rt, d.k + d.S, (int)sh.tokens, d.dtype, o, inv, s), "combine");
 }
 
 int set_error(int code, const char* fmt, ...) {

@@ -54,7 +54,9 @@ struct Row8<bf16_t> {
 // SPLIT (bf16 only): o is not stored; its rows are formed from the two fp32
 // K halves of the down GEMM at part and part + stride, rounded as the
 // split-K sum rounds them, so the result is the same bit for bit.
-template <typename TO, class RTA, bool SPLIT = false>
+// NS: slots the kernel holds rows for (k + S <= NS); sized to the stack so
+// that small k + S keeps few registers and many wavefronts per SIMD.
+template <typename TO, class RTA, bool SPLIT, int NS>
 __global__ __launch_bounds__(kCombThreads) void combine_kernel(RTA rta, const TO* __restrict__ o,
                                                                const int32_t* __restrict__ inv,
                                                                const float* __restrict__ part = nullptr,
@@ -76,9 +78,9 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(RTA rta, const TO
   __syncthreads();
   float* x = rt.x[rho] + (size_t)t * H;
   for (int c = threadIdx.x * 8; c < H; c += kCombThreads * 8) {
-    Row8<TO> v[kMaxSlots];
+    Row8<TO> v[NS];
 #pragma unroll
-    for (int r = 0; r < kMaxSlots; ++r)
+    for (int r = 0; r < NS; ++r)
       if (r < slots) {
         if constexpr (SPLIT)
           v[r].load_split(part + (size_t)s_row[r] * H + c, stride);
@@ -89,7 +91,7 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(RTA rta, const TO
     float4 x1 = reinterpret_cast<float4*>(x + c)[1];
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int r = 0; r < kMaxSlots; ++r) {
+    for (int r = 0; r < NS; ++r) {
       if (r < k) {
         const float wr = s_w[r];
 #pragma unroll
@@ -110,16 +112,31 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(RTA rta, const TO
 
 namespace {
 
+// Launch with the smallest slot capacity that holds k + S.
+template <typename TO, class RTA, bool SPLIT>
+void combine_launch(int slots, int grid_tokens, RTA a, const TO* o, const int32_t* inv, const float* part,
+                    long long stride, hipStream_t s) {
+  const dim3 grid(grid_tokens), block(kCombThreads);
+  if (slots <= 2)
+    hipLaunchKernelGGL((combine_kernel<TO, RTA, SPLIT, 2>), grid, block, 0, s, a, o, inv, part, stride);
+  else if (slots <= 4)
+    hipLaunchKernelGGL((combine_kernel<TO, RTA, SPLIT, 4>), grid, block, 0, s, a, o, inv, part, stride);
+  else if (slots <= 8)
+    hipLaunchKernelGGL((combine_kernel<TO, RTA, SPLIT, 8>), grid, block, 0, s, a, o, inv, part, stride);
+  else
+    hipLaunchKernelGGL((combine_kernel<TO, RTA, SPLIT, kMaxSlots>), grid, block, 0, s, a, o, inv, part, stride);
+}
+
 template <class RTA>
-void combine_impl(RTA a, int grid_tokens, int dtype, const void* o, const int32_t* inv, hipStream_t s) {
+void combine_impl(RTA a, int slots, int grid_tokens, int dtype, const void* o, const int32_t* inv,
+                  hipStream_t s) {
   prof_start(EB_K_COMBINE, s);
   if (grid_tokens > 0) {
     if (dtype == EB_DTYPE_BF16)
-      hipLaunchKernelGGL((combine_kernel<bf16_t, RTA>), dim3(grid_tokens), dim3(kCombThreads), 0, s, a,
-                         static_cast<const bf16_t*>(o), inv);
+      combine_launch<bf16_t, RTA, false>(slots, grid_tokens, a, static_cast<const bf16_t*>(o), inv, nullptr, 0,
+                                         s);
     else
-      hipLaunchKernelGGL((combine_kernel<float, RTA>), dim3(grid_tokens), dim3(kCombThreads), 0, s, a,
-                         static_cast<const float*>(o), inv);
+      combine_launch<float, RTA, false>(slots, grid_tokens, a, static_cast<const float*>(o), inv, nullptr, 0, s);
   }
   prof_stop(EB_K_COMBINE, s);
 }
@@ -128,22 +145,22 @@ void combine_impl(RTA a, int grid_tokens, int dtype, const void* o, const int32_
 
 hipError_t launch_combine(const RunTable& rt, int dtype, const void* o, const int32_t* inv,
                           hipStream_t s) {
-  combine_impl(ByValue<RunTable>{rt}, rt.tok_base[rt.n], dtype, o, inv, s);
+  combine_impl(ByValue<RunTable>{rt}, rt.k + rt.S, rt.tok_base[rt.n], dtype, o, inv, s);
   return hipGetLastError();
 }
 
-hipError_t launch_combine_dev(const RunTable* rt, int max_tokens, int dtype, const void* o,
+hipError_t launch_combine_dev(const RunTable* rt, int slots, int max_tokens, int dtype, const void* o,
                               const int32_t* inv, hipStream_t s) {
-  combine_impl(InMemory<RunTable>{rt}, max_tokens, dtype, o, inv, s);
+  combine_impl(InMemory<RunTable>{rt}, slots, max_tokens, dtype, o, inv, s);
   return hipGetLastError();
 }
 
-hipError_t launch_combine_split_dev(const RunTable* rt, int max_tokens, const float* part, long long stride,
-                                    const int32_t* inv, hipStream_t s) {
+hipError_t launch_combine_split_dev(const RunTable* rt, int slots, int max_tokens, const float* part,
+                                    long long stride, const int32_t* inv, hipStream_t s) {
   prof_start(EB_K_COMBINE, s);
   if (max_tokens > 0)
-    hipLaunchKernelGGL((combine_kernel<bf16_t, InMemory<RunTable>, true>), dim3(max_tokens), dim3(kCombThreads),
-                       0, s, InMemory<RunTable>{rt}, static_cast<const bf16_t*>(nullptr), inv, part, stride);
+    combine_launch<bf16_t, InMemory<RunTable>, true>(slots, max_tokens, InMemory<RunTable>{rt}, nullptr, inv, part,
+                                                     stride, s);
   prof_stop(EB_K_COMBINE, s);
   return hipGetLastError();
 }

@@ -215,11 +215,12 @@ hipError_t launch_down(int dtype, const GroupedProblem& p, const WeightTable& wt
 
 hipError_t launch_combine(const RunTable& rt, int dtype, const void* o, const int32_t* inv,
                           hipStream_t s);
-hipError_t launch_combine_dev(const RunTable* rt, int max_tokens, int dtype, const void* o,
+hipError_t launch_combine_dev(const RunTable* rt, int slots, int max_tokens, int dtype, const void* o,
                               const int32_t* inv, hipStream_t s);
 // bf16 combine straight from a split-K down GEMM's fp32 halves (part and
-// part + stride), rounded as the split-K sum would round them.
-hipError_t launch_combine_split_dev(const RunTable* rt, int max_tokens, const float* part, long long stride,
+// part + stride), rounded as the split-K sum would round them.  slots: k + S
+// (the device-resident table's, known to the caller).
+hipError_t launch_combine_split_dev(const RunTable* rt, int slots, int max_tokens, const float* part, long long stride,
                                     const int32_t* inv, hipStream_t s);
 
 // Profiling hooks (api.cpp): bracket one launch of kernel class `kind`.
