@@ -37,7 +37,8 @@ STEP_IDS = IDS + [LONGK.name + "_longk", ROWONCE.name + "_rowonce"]
 #   with rows long enough for the read-once grouping;
 # * k = E (every token on every expert), bf16 and fp32;
 # * L * (E + S) = 15360 keys in one step's grouping, with E = 252 experts
-#   (not a multiple of the router's 32-expert blocks)
+#   (not a multiple of the router's 32-expert blocks);
+# * 100 experts (the router's form for 65..128 experts)
 MAXSLOTS = Config("maxslots_bf16", L=2, H=256, F=256, E=64, k=12, S=4, D=8, N=4, T=96, dtype="bf16",
                   skew="zipf", skew_param=1.1, seed=20261001)
 LIMIT_CFGS = [
@@ -49,6 +50,10 @@ LIMIT_CFGS = [
            skew="dirichlet", skew_param=0.3, seed=20261004),
     Config("maxkeys_bf16", L=60, H=256, F=128, E=252, k=2, S=4, D=4, N=4, T=48, dtype="bf16",
            skew="zipf", skew_param=1.2, seed=20261005),
+    # 65..128 experts: the router's one-expert-block-per-wavefront form, a
+    # 128-token tile plus a ragged one
+    Config("experts100_bf16", L=2, H=512, F=256, E=100, k=6, S=2, D=4, N=3, T=150, dtype="bf16",
+           skew="dirichlet", skew_param=0.3, seed=20261006),
 ]
 LIMIT_IDS = [c.name for c in LIMIT_CFGS]
 
