@@ -54,6 +54,14 @@ LIMIT_CFGS = [
     # 128-token tile plus a ragged one
     Config("experts100_bf16", L=2, H=512, F=256, E=100, k=6, S=2, D=4, N=3, T=150, dtype="bf16",
            skew="dirichlet", skew_param=0.3, seed=20261006),
+    # fp32 routing paths: the per-token kernel with rows over 4096 wide and
+    # with 9..64 experts, and the separate logits and top-k kernels above 64
+    Config("wide_f32", L=2, H=6144, F=128, E=8, k=2, S=0, D=4, N=2, T=40, dtype="f32",
+           skew="zipf", skew_param=1.2, seed=20261007),
+    Config("experts40_f32", L=2, H=256, F=128, E=40, k=4, S=1, D=8, N=3, T=70, dtype="f32",
+           skew="zipf", skew_param=1.1, seed=20261008),
+    Config("experts96_f32", L=2, H=256, F=128, E=96, k=3, S=0, D=4, N=3, T=70, dtype="f32",
+           skew="dirichlet", skew_param=0.3, seed=20261009),
 ]
 LIMIT_IDS = [c.name for c in LIMIT_CFGS]
 
