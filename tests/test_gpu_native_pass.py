@@ -20,6 +20,11 @@ SMALL = ([c if c.dtype == "f32" else mini(c) for c in CONFIGS]
          + [mini(BY_NAME["mixtral_bf16"], H=256, F=8192, T=96, L=2),
             mini(BY_NAME["dsv3_share_bf16"], H=2048, T=96, L=2)])
 SMALL_IDS = [c.name for c in SMALL[:-2]] + [SMALL[-2].name + "_longk", SMALL[-1].name + "_rowonce"]
+# the device scheduler's 16- and 64-device forms (the stacks above use 4, 8
+# and 32 virtual devices)
+SMALL += [mini(BY_NAME["qwen_moe_bf16"], E=64, D=16, H=256, F=128, T=96, L=3).scaled(name="d16_bf16"),
+          mini(BY_NAME["dsv3_share_bf16"], E=128, D=64, H=256, F=128, T=96, L=3).scaled(name="d64_bf16")]
+SMALL_IDS += ["d16", "d64"]
 
 
 def _compare(cfg, device, policies):
