@@ -301,17 +301,19 @@ def test_schedule_invariance_and_replay(cfg, device):
 
 
 # group sizes on both sides of every tile-shape boundary (64 / 128 / 256-row
-# m-tiles, 32-row MFMA blocks, rows split evenly over two wavefront rows)
+# m-tiles, 32-row MFMA blocks, rows split evenly over two wavefront rows),
+# and groups of more m-tiles than one block of the GEMM's item order (5 and 6
+# m-tiles: a block of four and a ragged one)
 EDGE_SIZES = [[150, 129, 193, 65, 33, 1, 287, 64], [160, 161, 192, 128, 127, 63, 31, 256],
-              [255, 257, 96, 32, 0, 97, 200, 3]]
+              [255, 257, 96, 32, 0, 97, 200, 3], [1100, 1500, 300, 0, 500, 7, 64, 1]]
 
 
 def test_moe_step_group_sizes_span_tile_shapes(device):
-    """Crafted routing (not the router's): three entries at different layers
+    """Crafted routing (not the router's): one entry per row of EDGE_SIZES, at different layers,
     whose (layer, expert) groups take every row count around the tile-shape
     boundaries; every row of h and o checked against the oracle."""
     B = _binding()
-    cfg = mini(BY_NAME["mixtral_bf16"], H=256, F=256, L=3)
+    cfg = mini(BY_NAME["mixtral_bf16"], H=256, F=256, L=len(EDGE_SIZES))
     assert cfg.k == 2 and cfg.E == 8 and cfg.S == 0
     log(f"group-size parity {cfg.name}")
     inp = ensure_packed(cfg, DeviceInputs(cfg, device))
