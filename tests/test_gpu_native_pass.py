@@ -63,6 +63,15 @@ def test_native_pass_full_size_bench_stack(device):
     _compare(cfg, device, [("maxutil", cfg.m), ("lockstep", None)])
 
 
+@pytest.mark.parametrize("name", ["qwen_moe_bf16", "dsv2_lite_bf16", "dsv3_share_bf16"])
+def test_native_pass_full_size_other_stacks(name, device):
+    """The pass bench.py times (native, host- and device-scheduled) against
+    the Python driver's, whose every step the full-size parity test checks
+    against the oracle: bit-identical hidden states, loads and steps."""
+    cfg = BY_NAME[name]
+    _compare(cfg, device, [("maxutil", cfg.m)])
+
+
 def test_native_pass_pool_over_32_micro_batches(device):
     """40 micro-batches: the routing after a step spans two batch tables
     (32 entries each), host- and device-scheduled (MaxUtil enumerates pools
