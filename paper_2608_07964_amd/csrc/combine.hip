@@ -73,10 +73,10 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(RTA rta, const TO
   const int P = total * slots;  // grouped rows; inv is clamped into [0, P)
   if (threadIdx.x < slots) {
     s_row[threadIdx.x] = min(max(inv[(size_t)g * slots + threadIdx.x], 0), P - 1);
-    s_w[threadIdx.x] = threadIdx.x < k ? rt.w[rho][(size_t)t * k + threadIdx.x] : 1.f;
+    s_w[threadIdx.x] = threadIdx.x < k ? in_global(rt.w[rho])[(size_t)t * k + threadIdx.x] : 1.f;
   }
   __syncthreads();
-  float* x = rt.x[rho] + (size_t)t * H;
+  float* x = in_global(rt.x[rho]) + (size_t)t * H;
   for (int c = threadIdx.x * 8; c < H; c += kCombThreads * 8) {
     Row8<TO> v[NS];
 #pragma unroll

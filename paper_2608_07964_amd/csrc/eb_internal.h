@@ -81,6 +81,18 @@ __device__ __forceinline__ int find_entry(const int32_t* base, int n, int v) {
   return lo;
 }
 
+// A pointer read from a table in device memory is a generic address to the
+// compiler, so its loads and stores become flat instructions, which also
+// count on the LDS counter (every wait for them waits for LDS traffic too,
+// and the other way round).  Every table pointer here points into device
+// global memory; rebuilt from its integer value in the global address space,
+// it (and every pointer derived from it) gets global loads and stores; a
+// null pointer stays null.
+template <class T>
+__device__ __forceinline__ T* in_global(T* p) {
+  return (T*)(__attribute__((address_space(1))) T*)(uintptr_t)p;
+}
+
 // Routing of up to kRouteBatch micro-batches in one set of launches: entry i
 // holds tokens tok0[i] .. tok0[i+1]-1 of the batch and 32-token blocks
 // blk0[i] .. blk0[i+1]-1; gain/Wg/bias are those of the entry's layer.

@@ -42,7 +42,7 @@ __global__ __launch_bounds__(kPermChunk) void perm_count_kernel(RTA rta, int32_t
   const int T = rt.tok_base[rho + 1] - rt.tok_base[rho];
   const int t = (b - rt.chunk_base[rho]) * kPermChunk + threadIdx.x;
   if (t < T) {
-    const int32_t* ix = rt.idx[rho] + (size_t)t * rt.k;
+    const int32_t* ix = in_global(rt.idx[rho]) + (size_t)t * rt.k;
     for (int r = 0; r < rt.k; ++r) atomicAdd(&cnt[clamp_expert(ix[r], rt.E)], 1);
   }
   __syncthreads();
@@ -224,7 +224,7 @@ __global__ __launch_bounds__(kPermChunk) void perm_scatter_kernel(
   const int t0 = (b - rt.chunk_base[rho]) * kPermChunk;
   const int t = t0 + threadIdx.x;
   const bool valid = t < T;
-  const int32_t* ix = rt.idx[rho] + (size_t)t * k;
+  const int32_t* ix = in_global(rt.idx[rho]) + (size_t)t * k;
   if (valid)
     for (int r = 0; r < k; ++r) atomicOr(&mask[wave][clamp_expert(ix[r], E)], 1ull << lane);
   __syncthreads();
@@ -264,7 +264,7 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(RTA rta, int elem_byte
   const int rho = find_entry(rt.tok_base, rt.n, g);
   const int t = g - rt.tok_base[rho];
   const size_t row_bytes = (size_t)rt.H * elem_bytes;
-  const uint4* src = reinterpret_cast<const uint4*>(static_cast<const uint8_t*>(rt.a[rho]) + (size_t)t * row_bytes);
+  const uint4* src = reinterpret_cast<const uint4*>(in_global(static_cast<const uint8_t*>(rt.a[rho])) + (size_t)t * row_bytes);
   uint4* dst = reinterpret_cast<uint4*>(a_perm + (size_t)p * row_bytes);
   const int n16 = (int)(row_bytes / 16);
   for (int c = lane; c < n16; c += 64) dst[c] = src[c];
@@ -292,7 +292,7 @@ __global__ __launch_bounds__(256) void gather_tokens_kernel(RTA rta, int pieces,
   const int rho = find_entry(rt.tok_base, rt.n, g);
   const int t = g - rt.tok_base[rho];
   const size_t row_bytes = (size_t)rt.H * elem_bytes;
-  const uint4* src = reinterpret_cast<const uint4*>(static_cast<const uint8_t*>(rt.a[rho]) + (size_t)t * row_bytes);
+  const uint4* src = reinterpret_cast<const uint4*>(in_global(static_cast<const uint8_t*>(rt.a[rho])) + (size_t)t * row_bytes);
   // lane r < slots holds the grouped position of slot r (clamped into range)
   const int pos = lane < slots ? min(max(inv[(size_t)g * slots + lane], 0), P - 1) : 0;
   const int n16 = (int)(row_bytes / 16);

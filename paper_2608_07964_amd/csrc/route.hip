@@ -78,9 +78,9 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(RBA rba, int H, float eps)
   if (g >= rb.tok0[rb.n]) return;
   const int ei = find_entry(rb.tok0, rb.n, g);
   const int t = g - rb.tok0[ei];
-  const float* __restrict__ x = rb.e[ei].x;
-  const float* __restrict__ gain = rb.e[ei].gain;
-  TA* __restrict__ a = static_cast<TA*>(rb.e[ei].a);
+  const float* __restrict__ x = in_global(rb.e[ei].x);
+  const float* __restrict__ gain = in_global(rb.e[ei].gain);
+  TA* __restrict__ a = in_global(static_cast<TA*>(rb.e[ei].a));
   const float4* xr = reinterpret_cast<const float4*>(x + (size_t)t * H);
   const float4* g4 = reinterpret_cast<const float4*>(gain);
   const int n4 = H >> 2;
@@ -275,8 +275,8 @@ __global__ __launch_bounds__(1024) void counts_kernel(RBA rba, int k, int E) {
   const int ei = blockIdx.x;
   if (ei >= rb.n) return;  // past the live entries (grid sized for a full batch)
   const int n = (rb.tok0[ei + 1] - rb.tok0[ei]) * k;
-  const int32_t* __restrict__ idx = rb.e[ei].idx;
-  int32_t* __restrict__ counts = rb.e[ei].counts;
+  const int32_t* __restrict__ idx = in_global(rb.e[ei].idx);
+  int32_t* __restrict__ counts = in_global(rb.e[ei].counts);
   __shared__ int hist[1024];
   for (int e = threadIdx.x; e < E; e += blockDim.x) hist[e] = 0;
   __syncthreads();
@@ -346,11 +346,24 @@ __global__ __launch_bounds__(256) void logits_kernel(int T, int H, int E, const 
 // Thread tid owns the 8-element chunks starting at h = 8 (tid + 256 i), held
 // in registers; per chunk it forms and stores the a values and adds their
 // (stored, rounded) values times every router row into one accumulator per
-// expert.  Sums of squares and logits are reduced by a butterfly per
-// wavefront and then over the 4 wavefronts in order; wavefront 0 adds the
-// bias and picks the top-k.
+// expert.  Sums of squares are reduced by a butterfly per wavefront and then
+// over the 4 wavefronts in order, and so are the logits; with E <= 8 the
+// per-wavefront logit sums take a reduce-scatter instead (10 lane exchanges
+// for the 8 sums rather than 48), the router rows of a chunk are loaded
+// together, and 8 lanes of wavefront 0 pick the top-k; otherwise thread 0
+// picks it.
 template <typename TA> struct Vec8;
 template <> struct Vec8<bf16_t> {
+  using Raw = uint4;
+  __device__ static __forceinline__ Raw load_raw(const bf16_t* p) { return *reinterpret_cast<const uint4*>(p); }
+  __device__ static __forceinline__ void unpack(const Raw& u, float (&f)[8]) {
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      f[2 * q] = __uint_as_float(w[q] << 16);
+      f[2 * q + 1] = __uint_as_float(w[q] & 0xffff0000u);
+    }
+  }
   // 8 bf16 of a router row / of a
   __device__ static __forceinline__ void load(const bf16_t* p, float (&f)[8]) {
     const uint4 u = *reinterpret_cast<const uint4*>(p);
@@ -375,6 +388,13 @@ template <> struct Vec8<bf16_t> {
   }
 };
 template <> struct Vec8<float> {
+  struct Raw { float4 u, v; };
+  __device__ static __forceinline__ Raw load_raw(const float* p) {
+    return Raw{reinterpret_cast<const float4*>(p)[0], reinterpret_cast<const float4*>(p)[1]};
+  }
+  __device__ static __forceinline__ void unpack(const Raw& r, float (&f)[8]) {
+    f[0] = r.u.x; f[1] = r.u.y; f[2] = r.u.z; f[3] = r.u.w; f[4] = r.v.x; f[5] = r.v.y; f[6] = r.v.z; f[7] = r.v.w;
+  }
   __device__ static __forceinline__ void load(const float* p, float (&f)[8]) {
     const float4 u = reinterpret_cast<const float4*>(p)[0], v = reinterpret_cast<const float4*>(p)[1];
     f[0] = u.x; f[1] = u.y; f[2] = u.z; f[3] = u.w; f[4] = v.x; f[5] = v.y; f[6] = v.z; f[7] = v.w;
@@ -401,14 +421,14 @@ __global__ __launch_bounds__(256, KC == 2 ? 8 : 1) void route_token_kernel(RBA r
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int ei = find_entry(rb.tok0, rb.n, blockIdx.x);
   const int t = blockIdx.x - rb.tok0[ei];
-  const float* __restrict__ x = rb.e[ei].x;
-  const float* __restrict__ gain = rb.e[ei].gain;
-  const TA* __restrict__ Wg = static_cast<const TA*>(rb.e[ei].Wg);
-  const float* __restrict__ bias = rb.e[ei].bias;
-  TA* __restrict__ a = static_cast<TA*>(rb.e[ei].a);
-  float* __restrict__ z = rb.e[ei].z;
-  int32_t* __restrict__ idx = rb.e[ei].idx;
-  float* __restrict__ w = rb.e[ei].w;
+  const float* __restrict__ x = in_global(rb.e[ei].x);
+  const float* __restrict__ gain = in_global(rb.e[ei].gain);
+  const TA* __restrict__ Wg = in_global(static_cast<const TA*>(rb.e[ei].Wg));
+  const float* __restrict__ bias = in_global(rb.e[ei].bias);
+  TA* __restrict__ a = in_global(static_cast<TA*>(rb.e[ei].a));
+  float* __restrict__ z = in_global(rb.e[ei].z);
+  int32_t* __restrict__ idx = in_global(rb.e[ei].idx);
+  float* __restrict__ w = in_global(rb.e[ei].w);
   const float* xr = x + (size_t)t * H;
   const int nchunk = H >> 3;
   // thread tid owns chunks c = tid + 256 i (8 elements each), kept in registers
@@ -449,34 +469,87 @@ __global__ __launch_bounds__(256, KC == 2 ? 8 : 1) void route_token_kernel(RBA r
 #pragma unroll
       for (int q = 0; q < 8; ++q) av[q] = xs[i][q] * r * g[q];
       Vec8<TA>::store_round(ar + h, av);  // the stored (rounded) values feed the router
+      if constexpr (EMAX == 8) {
+        // the router rows in batches of RB whose loads are in flight together
+        // (rows past E repeat row E-1; their sums are never used)
+        constexpr int RB = sizeof(TA) == 2 ? 8 : 2;
 #pragma unroll
-      for (int e = 0; e < EMAX; ++e) {
-        if (e < E) {
-          float wv[8];
-          Vec8<TA>::load(Wg + (size_t)e * H + h, wv);
+        for (int e0 = 0; e0 < 8; e0 += RB) {
+          typename Vec8<TA>::Raw wr[RB];
 #pragma unroll
-          for (int q = 0; q < 8; ++q) acc[e] = fmaf(av[q], wv[q], acc[e]);
+          for (int j = 0; j < RB; ++j) wr[j] = Vec8<TA>::load_raw(Wg + (size_t)min(e0 + j, E - 1) * H + h);
+#pragma unroll
+          for (int j = 0; j < RB; ++j) {
+            float wv[8];
+            Vec8<TA>::unpack(wr[j], wv);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) acc[e0 + j] = fmaf(av[q], wv[q], acc[e0 + j]);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < EMAX; ++e) {
+          if (e < E) {
+            float wv[8];
+            Vec8<TA>::load(Wg + (size_t)e * H + h, wv);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) acc[e] = fmaf(av[q], wv[q], acc[e]);
+          }
         }
       }
     }
   }
+  if constexpr (EMAX == 8) {
+    // the wavefront's 8 sums by a reduce-scatter over the lane bits 5, 4, 3
+    // (each step halves the sums a lane carries), then a butterfly over bits
+    // 2..0: lanes 8e .. 8e+7 end with the total of expert e
+    const bool b5 = lane & 32, b4 = lane & 16, b3 = lane & 8;
+    float r1[4], r2[2];
 #pragma unroll
-  for (int e = 0; e < EMAX; ++e) {
-    if (e < E) {
-      const float v = wave_sum(acc[e]);
-      if (lane == 0) red_z[wave][e] = v;
+    for (int j = 0; j < 4; ++j) {
+      const float give = b5 ? acc[j] : acc[j + 4];
+      r1[j] = (b5 ? acc[j + 4] : acc[j]) + __shfl_xor(give, 32, 64);  // expert j + 4 b5
     }
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const float give = b4 ? r1[j] : r1[j + 2];
+      r2[j] = (b4 ? r1[j + 2] : r1[j]) + __shfl_xor(give, 16, 64);  // expert j + 2 b4 + 4 b5
+    }
+    float r3 = (b3 ? r2[1] : r2[0]) + __shfl_xor(b3 ? r2[0] : r2[1], 8, 64);
+#pragma unroll
+    for (int off = 4; off > 0; off >>= 1) r3 += __shfl_xor(r3, off, 64);
+    const int e = lane >> 3;
+    if ((lane & 7) == 0 && e < E) red_z[wave][e] = r3;
+    __syncthreads();
+    // lanes 0..7 of wavefront 0: logit of expert `lane` (the 4 wavefronts'
+    // sums in order, then the bias), then the top-k over the 8 lanes
+    if (tid < 8) {
+      if (tid < E) {
+        const float ze = (((red_z[0][tid] + red_z[1][tid]) + red_z[2][tid]) + red_z[3][tid]) + bias[tid];
+        red_z[0][tid] = ze;  // read back by this lane only
+        if (z != nullptr) z[(size_t)t * E + tid] = ze;
+      }
+      topk_group8<1, 8>(tid, E, k, norm_topk, red_z[0], idx + (size_t)t * k, w + (size_t)t * k);
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < EMAX; ++e) {
+      if (e < E) {
+        const float v = wave_sum(acc[e]);
+        if (lane == 0) red_z[wave][e] = v;
+      }
+    }
+    __syncthreads();
+    if (tid < E) {
+      const float ze = (((red_z[0][tid] + red_z[1][tid]) + red_z[2][tid]) + red_z[3][tid]) + bias[tid];
+      red_z[0][tid] = ze;  // each thread rewrites only its own entry
+      if (z != nullptr) z[(size_t)t * E + tid] = ze;
+    }
+    __syncthreads();
+    if (tid == 0)
+      topk_token(E, k, norm_topk, [&](int e) { return red_z[0][e]; }, idx + (size_t)t * k,
+                 w + (size_t)t * k);
   }
-  __syncthreads();
-  if (tid < E) {
-    const float ze = (((red_z[0][tid] + red_z[1][tid]) + red_z[2][tid]) + red_z[3][tid]) + bias[tid];
-    red_z[0][tid] = ze;  // each thread rewrites only its own entry
-    if (z != nullptr) z[(size_t)t * E + tid] = ze;
-  }
-  __syncthreads();
-  if (tid == 0)
-    topk_token(E, k, norm_topk, [&](int e) { return red_z[0][e]; }, idx + (size_t)t * k,
-               w + (size_t)t * k);
 }
 
 // ---------------------------------------------------------------------------
@@ -501,12 +574,12 @@ __global__ __launch_bounds__(256) void route_mfma_kernel(RBA rba, int H, int E, 
   const int ei = find_entry(rb.blk0, rb.n, blockIdx.x);
   const int T = rb.tok0[ei + 1] - rb.tok0[ei];
   const int t0 = (blockIdx.x - rb.blk0[ei]) * 32;
-  const bf16_t* __restrict__ a = static_cast<const bf16_t*>(rb.e[ei].a);
-  const bf16_t* __restrict__ Wg = static_cast<const bf16_t*>(rb.e[ei].Wg);
-  const float* __restrict__ bias = rb.e[ei].bias;
-  float* __restrict__ z = rb.e[ei].z;
-  int32_t* __restrict__ idx = rb.e[ei].idx;
-  float* __restrict__ w = rb.e[ei].w;
+  const bf16_t* __restrict__ a = in_global(static_cast<const bf16_t*>(rb.e[ei].a));
+  const bf16_t* __restrict__ Wg = in_global(static_cast<const bf16_t*>(rb.e[ei].Wg));
+  const float* __restrict__ bias = in_global(rb.e[ei].bias);
+  float* __restrict__ z = in_global(rb.e[ei].z);
+  int32_t* __restrict__ idx = in_global(rb.e[ei].idx);
+  float* __restrict__ w = in_global(rb.e[ei].w);
   const int kq = H / 4, kbeg = wave * kq;
   // this lane's A row (token) and B rows (experts), clamped into range
   const bf16_t* arow = a + (size_t)min(t0 + lrow, T - 1) * H + kbeg + 8 * khalf;
@@ -636,12 +709,12 @@ __global__ __launch_bounds__(512) void route_lds_kernel(RBA rba, int H, int E, i
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wave >> 2, wn = wave & 3;
   const int lrow = lane & 31, khalf = lane >> 5;
-  const bf16_t* __restrict__ a = static_cast<const bf16_t*>(rb.e[ei].a);
-  const bf16_t* __restrict__ Wg = static_cast<const bf16_t*>(rb.e[ei].Wg);
-  const float* __restrict__ bias = rb.e[ei].bias;
-  float* __restrict__ z = rb.e[ei].z;
-  int32_t* __restrict__ idx = rb.e[ei].idx;
-  float* __restrict__ w = rb.e[ei].w;
+  const bf16_t* __restrict__ a = in_global(static_cast<const bf16_t*>(rb.e[ei].a));
+  const bf16_t* __restrict__ Wg = in_global(static_cast<const bf16_t*>(rb.e[ei].Wg));
+  const float* __restrict__ bias = in_global(rb.e[ei].bias);
+  float* __restrict__ z = in_global(rb.e[ei].z);
+  int32_t* __restrict__ idx = in_global(rb.e[ei].idx);
+  float* __restrict__ w = in_global(rb.e[ei].w);
   // buffer descriptors: rows past the tokens' or the experts' end read zeros
   const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<bf16_t*>(a + (size_t)t0 * H), (short)0, min(T - t0, kRouteTokens) * H * 2, 0x00020000);
