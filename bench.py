@@ -238,17 +238,14 @@ def main() -> int:
     # algorithmic HBM bytes per pass of the memory-bound kernels (and the down
     # GEMM) against the 8 TB/s peak, from the per-kernel event times above
     tokens_pass = cfg.N * cfg.T * cfg.L            # every (micro-batch, layer) routed once
-    slots = cfg.k + cfg.S
     router_bytes = cfg.E * cfg.H * eb
     alg_bytes = {
         # x read (fp32), a written, logits / picks / weights written, each
         # launch's router rows read once
         "route_logits": tokens_pass * (4 * cfg.H + eb * cfg.H + 4 * cfg.E + 8 * cfg.k)
                         + prof_all["route_logits"][1] / n_bd * router_bytes,
-        # grouped rows: a row read and written per pair (per-token form: the
-        # token's row read once, written per pair)
-        "perm_gather": (pairs_pass * 2 * cfg.H * eb if (slots - 1) * cfg.H * eb < 32768
-                        else (tokens_pass + pairs_pass) * cfg.H * eb),
+        # grouped rows: a token's row read once, written per pair
+        "perm_gather": (tokens_pass + pairs_pass) * cfg.H * eb,
         # o rows read per pair, x read and written per token, weights and rows
         "combine": pairs_pass * (cfg.H * eb + 8) + tokens_pass * 8 * cfg.H,
         # weights of the distinct groups, h read, o written

@@ -13,10 +13,9 @@
 //   perm_scatter_kernel  per chunk: stable rank of each pair inside its key from
 //                        per-wavefront 64-bit expert masks (popcount of the lanes
 //                        below), then inv and perm
-//   gather_rows_kernel   one wavefront per grouped row: a_perm[p] = a of perm[p]
-//   gather_tokens_kernel (many pairs of long rows) one wavefront per (token,
-//                        2 KB piece of its row): the piece, read once, to
-//                        a_perm[inv[q]] for each of the token's k+S pairs q
+//   gather_tokens_kernel one wavefront per (token, 1 KB piece of its row):
+//                        the piece, read once, to a_perm[inv[q]] for each of
+//                        the token's k+S pairs q
 //
 // Pair q = (tok_base[rho] + t) * (k+S) + r; key = layer*(E+S) + slot expert.
 // All results are integers fixed by the inputs (no order-dependent atomics).
@@ -248,32 +247,12 @@ __global__ __launch_bounds__(kPermChunk) void perm_scatter_kernel(
   }
 }
 
-// One wavefront per grouped row: a_perm[p] = a of perm[p].  A token's row is
-// read once per pair; used when a token has few pairs or short rows.
-template <class RTA>
-__global__ __launch_bounds__(256) void gather_rows_kernel(RTA rta, int elem_bytes,
-                                                          const int32_t* __restrict__ perm,
-                                                          uint8_t* __restrict__ a_perm) {
-  const RunTable& rt = rta.get();
-  const int lane = threadIdx.x & 63;
-  const int p = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int slots = rt.k + rt.S;
-  const int P = rt.tok_base[rt.n] * slots;
-  if (p >= P) return;
-  const int g = min(max(perm[p], 0), P - 1) / slots;  // global token of the pair
-  const int rho = find_entry(rt.tok_base, rt.n, g);
-  const int t = g - rt.tok_base[rho];
-  const size_t row_bytes = (size_t)rt.H * elem_bytes;
-  const uint4* src = reinterpret_cast<const uint4*>(in_global(static_cast<const uint8_t*>(rt.a[rho])) + (size_t)t * row_bytes);
-  uint4* dst = reinterpret_cast<uint4*>(a_perm + (size_t)p * row_bytes);
-  const int n16 = (int)(row_bytes / 16);
-  for (int c = lane; c < n16; c += 64) dst[c] = src[c];
-}
-
-// One wavefront per (token, 2 KB piece of its row): the piece is read once
-// (two 16-byte loads per lane) and written to the grouped positions inv[q]
-// of all the token's k+S pairs.
-constexpr int kGatherU = 2;                  // 16-byte loads per lane per piece
+// One wavefront per (token, 1 KB piece of its row): the piece is read once
+// (one 16-byte load per lane) and written to the grouped positions inv[q]
+// of all the token's k+S pairs.  Reading each row once per pair instead (one
+// wavefront per grouped row) moves up to k+S times the read bytes; pieces of
+// 2 KB keep fewer wavefronts in flight.
+constexpr int kGatherU = 1;                  // 16-byte loads per lane per piece
 constexpr int kGatherPiece = 64 * kGatherU;  // 16-byte chunks per piece
 
 template <class RTA>
@@ -335,14 +314,9 @@ void perm_scan_impl(RTA a, const int32_t* hist, int32_t* chunk_base, int32_t* of
   prof_stop(EB_K_PERM_SCAN, s);
 }
 
-// read each token's row once when that saves >= 32 KB of re-reads per
-// token (many pairs of long rows: the DeepSeek-V3 shape); else one
-// wavefront per grouped row, which keeps more wavefronts in flight
-bool gather_by_token(int slots, size_t row_bytes) { return (size_t)(slots - 1) * row_bytes >= 32768; }
-
 // grid_chunks / grid_tokens: chunks and tokens the grids cover
 template <class RTA>
-void perm_scatter_impl(RTA a, int slots, int H, int grid_chunks, int grid_tokens, int elem_bytes,
+void perm_scatter_impl(RTA a, int H, int grid_chunks, int grid_tokens, int elem_bytes,
                        const int32_t* chunk_base, int32_t* perm, int32_t* inv, void* a_perm,
                        hipStream_t s) {
   prof_start(EB_K_PERM_SCATTER, s);
@@ -353,17 +327,11 @@ void perm_scatter_impl(RTA a, int slots, int H, int grid_chunks, int grid_tokens
   const size_t row_bytes = (size_t)H * elem_bytes;
   prof_start(EB_K_PERM_GATHER, s);
   if (grid_tokens > 0) {
-    if (gather_by_token(slots, row_bytes)) {
-      const int n16 = (int)(row_bytes / 16);
-      const int pieces = (n16 + kGatherPiece - 1) / kGatherPiece;
-      const long long waves = (long long)grid_tokens * pieces;
-      hipLaunchKernelGGL(gather_tokens_kernel<RTA>, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s,
-                         a, pieces, elem_bytes, inv, static_cast<uint8_t*>(a_perm));
-    } else {
-      const long long P = (long long)grid_tokens * slots;
-      hipLaunchKernelGGL(gather_rows_kernel<RTA>, dim3((unsigned)((P + 3) / 4)), dim3(256), 0, s, a,
-                         elem_bytes, perm, static_cast<uint8_t*>(a_perm));
-    }
+    const int n16 = (int)(row_bytes / 16);
+    const int pieces = (n16 + kGatherPiece - 1) / kGatherPiece;
+    const long long waves = (long long)grid_tokens * pieces;
+    hipLaunchKernelGGL(gather_tokens_kernel<RTA>, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s, a,
+                       pieces, elem_bytes, inv, static_cast<uint8_t*>(a_perm));
   }
   prof_stop(EB_K_PERM_GATHER, s);
 }
@@ -392,7 +360,7 @@ hipError_t launch_perm_scan(const RunTable& rt, const int32_t* hist, int32_t* ch
 hipError_t launch_perm_scatter(const RunTable& rt, int n_chunks, int elem_bytes,
                                const int32_t* chunk_base, int32_t* perm, int32_t* inv,
                                void* a_perm, hipStream_t s) {
-  perm_scatter_impl(ByValue<RunTable>{rt}, rt.k + rt.S, rt.H, n_chunks, rt.tok_base[rt.n], elem_bytes,
+  perm_scatter_impl(ByValue<RunTable>{rt}, rt.H, n_chunks, rt.tok_base[rt.n], elem_bytes,
                     chunk_base, perm, inv, a_perm, s);
   return hipGetLastError();
 }
@@ -405,7 +373,7 @@ hipError_t launch_permute_dev(const eb_model_desc& d, const RunTable* rt, int ma
   perm_count_impl(a, max_chunks, b.hist, s);
   perm_scan_impl(a, b.hist, b.chunk_base, b.offsets, b.tiles, b.n_tiles, b.groups, b.n_groups,
                  gemm_bm(d.dtype), b.max_tiles, b.work_ctr, s);
-  perm_scatter_impl(a, d.k + d.S, d.H, max_chunks, max_tokens, eb, b.chunk_base, b.perm, b.inv,
+  perm_scatter_impl(a, d.H, max_chunks, max_tokens, eb, b.chunk_base, b.perm, b.inv,
                     b.a_perm, s);
   return hipGetLastError();
 }

@@ -14,8 +14,8 @@ from gpu_helpers import log, make_stack
 
 pytestmark = pytest.mark.gpu
 
-# plus a split-K down GEMM (F >= 8192) and the read-once gather (k+S = 9
-# slots of 4 KB rows)
+# plus a split-K down GEMM (F >= 8192) and many pairs of long rows in the
+# grouping (k+S = 9 slots of 4 KB rows: four pieces per token)
 SMALL = ([c if c.dtype == "f32" else mini(c) for c in CONFIGS]
          + [mini(BY_NAME["mixtral_bf16"], H=256, F=8192, T=96, L=2),
             mini(BY_NAME["dsv3_share_bf16"], H=2048, T=96, L=2)])

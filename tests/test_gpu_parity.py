@@ -27,14 +27,14 @@ MINIS = [c if c.dtype == "f32" else mini(c) for c in CONFIGS]
 IDS = [c.name for c in MINIS]
 # long K (F >= 8192): the down GEMM runs its two K halves as separate items
 LONGK = mini(BY_NAME["mixtral_bf16"], H=256, F=8192, T=96, L=2)
-# many pairs of long rows ((k+S-1) * H * 2 >= 32 KB): the grouping reads each
-# token's row once (gather_tokens_kernel)
+# many pairs of long rows (k+S = 9 slots of 4 KB rows): the grouping copies
+# each token's row piece by piece to all its pairs (gather_tokens_kernel)
 ROWONCE = mini(BY_NAME["dsv3_share_bf16"], H=2048, T=96, L=2)
 STEP_CFGS = MINIS + [LONGK, ROWONCE]
 STEP_IDS = IDS + [LONGK.name + "_longk", ROWONCE.name + "_rowonce"]
 # the ABI's shape limits and the method's degenerate mixtures:
 # * k + S = 16 expert slots per token (12 routed picks of 64, 4 shared), also
-#   with rows long enough for the read-once grouping;
+#   with rows of several pieces in the grouping;
 # * k = E (every token on every expert), bf16 and fp32;
 # * L * (E + S) = 15360 keys in one step's grouping, with E = 252 experts
 #   (not a multiple of the router's 32-expert blocks);
