@@ -3,16 +3,19 @@
 //                        per token computes a = dtype(x * r * gain),
 //                        z = a Wg^T + bias and the top-k with its softmax
 //                        weights
-//   rmsnorm_kernel +     other bf16 stacks: RMSNorm, then the router GEMM on
+//   RMSNorm +            other bf16 stacks: RMSNorm, then the router GEMM on
 //   route_mfma_kernel /  the matrix cores and the top-k of the workgroup's 32
 //   route_lds_kernel     tokens from an LDS logit tile (E <= 64: 32 tokens,
 //                        split-K over the 4 wavefronts, operands straight into
 //                        registers; E > 64: 128 tokens, 8 wavefronts splitting
 //                        tokens and experts, operands staged through LDS as
 //                        whole cache lines)
-//   rmsnorm_kernel +     other fp32 stacks: RMSNorm, an LDS-tiled fp32
+//   RMSNorm +            other fp32 stacks: RMSNorm, an LDS-tiled fp32
 //   logits_kernel +      VALU GEMM for z, then the top-k
 //   topk_kernel
+//   RMSNorm              rmsnorm_row_kernel (H <= 8192: one workgroup per
+//                        token, the row read once into registers) or
+//                        rmsnorm_kernel (one wavefront per token)
 //   counts_kernel        expert counts of each micro-batch from its picks
 // Every kernel takes a batch of micro-batches (possibly at different layers)
 // and finds its entry from its block index, so routing several micro-batches
@@ -338,6 +341,50 @@ __global__ __launch_bounds__(256) void logits_kernel(int T, int H, int E, const 
       const int e = e0 + tx + 16 * j;
       if (e < E) z[(size_t)t * E + e] = acc[i][j] + bias[e];
     }
+  }
+}
+
+// RMSNorm + cast, one workgroup of 256 threads per token for long rows:
+// thread t holds the float4 slices t + 256 v (v < NV) of the row in
+// registers, so x is read once.  Sums of squares: each thread over its
+// slices in order, a butterfly per wavefront, then the 4 wavefronts in order.
+template <typename TA, int NV, class RBA>
+__global__ __launch_bounds__(256) void rmsnorm_row_kernel(RBA rba, int H, float eps) {
+  __shared__ float red[4];
+  const RouteBatch& rb = rba.get();
+  const int g = blockIdx.x;
+  if (g >= rb.tok0[rb.n]) return;  // past the live tokens
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int ei = find_entry(rb.tok0, rb.n, g);
+  const int t = g - rb.tok0[ei];
+  const float4* xr = reinterpret_cast<const float4*>(in_global(rb.e[ei].x) + (size_t)t * H);
+  const float4* g4 = reinterpret_cast<const float4*>(in_global(rb.e[ei].gain));
+  TA* ar = in_global(static_cast<TA*>(rb.e[ei].a)) + (size_t)t * H;
+  const int n4 = H >> 2;
+  float4 v[NV], gv[NV];
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int i = tid + 256 * j;
+    if (i < n4) {
+      v[j] = xr[i];
+      gv[j] = g4[i];
+    }
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < NV; ++j)
+    if (tid + 256 * j < n4) {
+      ss = fmaf(v[j].x, v[j].x, ss); ss = fmaf(v[j].y, v[j].y, ss);
+      ss = fmaf(v[j].z, v[j].z, ss); ss = fmaf(v[j].w, v[j].w, ss);
+    }
+  ss = wave_sum(ss);
+  if (lane == 0) red[wave] = ss;
+  __syncthreads();
+  const float r = 1.0f / sqrtf((((red[0] + red[1]) + red[2]) + red[3]) / (float)H + eps);
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int i = tid + 256 * j;
+    if (i < n4) store4(ar + 4 * i, normed(v[j], r, gv[j]));
   }
 }
 
@@ -870,8 +917,18 @@ hipError_t route_batch_typed(const eb_model_desc& d, RBA rba, const RouteBatch* 
       prof_stop(EB_K_ROUTE_LOGITS, s);
     } else {
       prof_start(EB_K_ROUTE_NORM, s);
-      hipLaunchKernelGGL((rmsnorm_kernel<TA, RBA>), dim3((grid_tokens + 3) / 4), dim3(256), 0, s, rba, d.H,
-                         d.rms_eps);
+      if (d.H > 4096 && d.H <= 256 * 4 * 8)
+        hipLaunchKernelGGL((rmsnorm_row_kernel<TA, 8, RBA>), dim3(grid_tokens), dim3(256), 0, s, rba, d.H,
+                           d.rms_eps);
+      else if (d.H > 2048 && d.H <= 256 * 4 * 4)
+        hipLaunchKernelGGL((rmsnorm_row_kernel<TA, 4, RBA>), dim3(grid_tokens), dim3(256), 0, s, rba, d.H,
+                           d.rms_eps);
+      else if (d.H <= 256 * 4 * 2)
+        hipLaunchKernelGGL((rmsnorm_row_kernel<TA, 2, RBA>), dim3(grid_tokens), dim3(256), 0, s, rba, d.H,
+                           d.rms_eps);
+      else
+        hipLaunchKernelGGL((rmsnorm_kernel<TA, RBA>), dim3((grid_tokens + 3) / 4), dim3(256), 0, s, rba, d.H,
+                           d.rms_eps);
       prof_stop(EB_K_ROUTE_NORM, s);
       prof_start(EB_K_ROUTE_LOGITS, s);
       if (sizeof(TA) == 2) {
