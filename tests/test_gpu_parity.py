@@ -64,6 +64,18 @@ LIMIT_CFGS = [
            skew="dirichlet", skew_param=0.3, seed=20261009),
 ]
 LIMIT_IDS = [c.name for c in LIMIT_CFGS]
+# the RMSNorm in front of the separate router kernels, by row length: a
+# workgroup per token holding 4 float4 of the row per thread (2048 < H <=
+# 4096), 8 (4096 < H <= 8192), and one wavefront per token above that
+NORM_CFGS = [
+    Config("norm4_bf16", L=1, H=4096, F=128, E=64, k=4, S=0, D=4, N=2, T=70, dtype="bf16",
+           skew="zipf", skew_param=1.1, seed=20261010),
+    Config("norm8_f32", L=1, H=5120, F=128, E=96, k=3, S=0, D=4, N=2, T=70, dtype="f32",
+           skew="dirichlet", skew_param=0.3, seed=20261011),
+    Config("normwave_bf16", L=1, H=8448, F=128, E=100, k=6, S=0, D=4, N=2, T=70, dtype="bf16",
+           skew="dirichlet", skew_param=0.3, seed=20261012),
+]
+NORM_IDS = [c.name for c in NORM_CFGS]
 
 
 def _binding():
@@ -133,7 +145,7 @@ def test_device_generator_bit_exact(device):
             assert np.array_equal(t.cpu().numpy(), ref)
 
 
-@pytest.mark.parametrize("cfg", MINIS + LIMIT_CFGS, ids=IDS + LIMIT_IDS)
+@pytest.mark.parametrize("cfg", MINIS + LIMIT_CFGS + NORM_CFGS, ids=IDS + LIMIT_IDS + NORM_IDS)
 def test_route_stage(cfg, device):
     B = _binding()
     log(f"route parity {cfg.name}")
