@@ -180,36 +180,55 @@ __device__ __forceinline__ void topk_token(int E, int k, int norm_topk, ZRow zro
   else topk_thread<16>(E, k, norm_topk, zrow, idx_t, w_t);
 }
 
+// Order key of the logit v of expert e for the top-k: larger z first, then
+// lower id; NaN after every number (ties by id); -0 ranks as +0.  The float
+// maps to an unsigned integer of the same order (sign flipped for positive
+// values, all bits for negative ones), NaN to 1, and the id goes below it as
+// ~e, so a pick is one unsigned maximum.  Key 0 (below every expert) marks
+// padding.
+__device__ __forceinline__ uint64_t pick_key(float v, int e) {
+  uint32_t o = 1u;  // NaN
+  if (v == v) {
+    const uint32_t u = __float_as_uint(v == 0.f ? 0.f : v);
+    o = (u & 0x80000000u) ? ~u : (u | 0x80000000u);  // -inf -> 0x007fffff > 1
+  }
+  return ((uint64_t)o << 32) | (uint32_t)~(uint32_t)e;
+}
+__device__ __forceinline__ float key_value(uint64_t key) {
+  const uint32_t o = (uint32_t)(key >> 32);
+  if (o == 1u) return __builtin_nanf("");
+  return __uint_as_float((o & 0x80000000u) ? (o ^ 0x80000000u) : ~o);
+}
+
 // Top-k and softmax weights of one token by 8 consecutive lanes (sub = lane
-// % 8): lane sub holds the logits e = sub + 8 i (i < PER) and each pick is an
-// argmax over the 8 lanes' local bests under the same total order; the
-// softmax maximum and denominator are reduced over the 8 lanes in a fixed
-// pattern.  The picks stay in registers (k <= KMAX) and lane sub 0 writes
-// idx_t and w_t once.
+// % 8): lane sub holds the keys of the logits e = sub + 8 i (i < PER) and each
+// pick is the maximum key over the 8 lanes (the total order above: when only
+// NaN logits are left, the lowest unpicked id, so the k picks are distinct
+// experts); the softmax maximum and denominator are reduced over the 8 lanes
+// in a fixed pattern.  The picks stay in registers (k <= KMAX) and lane sub 0
+// writes idx_t and w_t once.
 template <int PER, int KMAX>
 __device__ __forceinline__ void topk_group8(int sub, int E, int k, int norm_topk, const float* zrow,
                                             int32_t* __restrict__ idx_t, float* __restrict__ w_t) {
   static_assert(PER <= 32, "taken mask");
-  float v[PER];
-  uint32_t taken = 0;
+  uint64_t key[PER];
+  uint32_t taken = 0;  // entries already picked
   float mx = -INFINITY;
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
     const int e = sub + 8 * i;
-    if (e < E) {
-      v[i] = zrow[e];
-      mx = fmaxf(mx, v[i]);
-    } else {
-      v[i] = -INFINITY;
-      taken |= 1u << i;
-    }
+    const float v = zrow[min(e, E - 1)];  // entries past E are padding
+    mx = fmaxf(mx, e < E ? v : -INFINITY);
+    key[i] = e < E ? pick_key(v, e) : 0ull;
   }
 #pragma unroll
   for (int off = 1; off < 8; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 8));
   float se = 0.f;
 #pragma unroll
-  for (int i = 0; i < PER; ++i)
-    if (!(taken & (1u << i))) se += expf(v[i] - mx);
+  for (int i = 0; i < PER; ++i) {
+    const float ev = expf(key_value(key[i]) - mx);
+    se += sub + 8 * i < E ? ev : 0.f;  // +0 leaves the (non-negative) sum's bits alone
+  }
 #pragma unroll
   for (int off = 1; off < 8; off <<= 1) se += __shfl_xor(se, off, 8);
   float esum = 0.f;
@@ -220,39 +239,21 @@ __device__ __forceinline__ void topk_group8(int sub, int E, int k, int norm_topk
     pw[r] = 0.f;
     pe[r] = 0;
     if (r < k) {
-      float bv = -INFINITY;
-      int be = E;  // sentinel: nothing selectable in this lane
+      uint64_t best = 0;
 #pragma unroll
       for (int i = 0; i < PER; ++i) {
-        const int e = sub + 8 * i;
-        if (!(taken & (1u << i)) && better(v[i], e, bv, be)) {
-          bv = v[i];
-          be = e;
-        }
+        const uint64_t ki = (taken >> i) & 1u ? 0ull : key[i];
+        best = ki > best ? ki : best;
       }
 #pragma unroll
       for (int off = 1; off < 8; off <<= 1) {
-        const float ov = __shfl_xor(bv, off, 8);
-        const int oe = __shfl_xor(be, off, 8);
-        if (better(ov, oe, bv, be)) {
-          bv = ov;
-          be = oe;
-        }
+        const uint64_t o = __shfl_xor(best, off, 8);
+        best = o > best ? o : best;
       }
-      if (be >= E) {
-        // every expert not yet picked has a NaN logit: the lowest such id
-        // (NaN ranks after every number, ties by id)
-        int lo = E;
-#pragma unroll
-        for (int i = PER - 1; i >= 0; --i)
-          if (!(taken & (1u << i))) lo = sub + 8 * i;
-#pragma unroll
-        for (int off = 1; off < 8; off <<= 1) lo = min(lo, __shfl_xor(lo, off, 8));
-        be = min(lo, E - 1);
-        bv = __builtin_nanf("");
-      }
+      int be = (int)~(uint32_t)best;
+      be = (be < 0 || be >= E) ? E - 1 : be;  // not reached: r < k <= E leaves an unpicked expert
       if ((be & 7) == sub) taken |= 1u << (be >> 3);
-      const float ev = expf(bv - mx);
+      const float ev = expf(key_value(best) - mx);
       esum += ev;
       pw[r] = ev;
       pe[r] = be;
