@@ -3,7 +3,8 @@
 // of Section 2.1):
 //   x[t] += sum_{r<k} w[t][r] * o[inv[q(t,r)]] + sum_{s<S} o[inv[q(t,k+s)]]
 // One workgroup per token; each thread owns 8 consecutive elements per pass
-// of 2048 and issues the loads of all k+S rows of a pass at once.  The sum is
+// of 2048 and issues the loads of all k+S rows of a pass at once (the
+// residual slice is read one pass ahead).  The sum is
 // formed in fp32 in slot order (routed ascending, then shared) before the
 // residual add, so each token's result is independent of the schedule.
 #include "eb_internal.h"
@@ -75,8 +76,15 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(RTA rta, const TO
     s_row[threadIdx.x] = min(max(inv[(size_t)g * slots + threadIdx.x], 0), P - 1);
     s_w[threadIdx.x] = threadIdx.x < k ? in_global(rt.w[rho])[(size_t)t * k + threadIdx.x] : 1.f;
   }
-  __syncthreads();
   float* x = in_global(rt.x[rho]) + (size_t)t * H;
+  // the residual slice of the first pass is read while inv is on its way,
+  // that of each next pass during the current one
+  float4 xn0 = make_float4(0.f, 0.f, 0.f, 0.f), xn1 = xn0;
+  if (threadIdx.x * 8 < H) {
+    xn0 = reinterpret_cast<float4*>(x + threadIdx.x * 8)[0];
+    xn1 = reinterpret_cast<float4*>(x + threadIdx.x * 8)[1];
+  }
+  __syncthreads();
   for (int c = threadIdx.x * 8; c < H; c += kCombThreads * 8) {
     Row8<TO> v[NS];
 #pragma unroll
@@ -87,8 +95,11 @@ __global__ __launch_bounds__(kCombThreads) void combine_kernel(RTA rta, const TO
         else
           v[r].load(o + (size_t)s_row[r] * H + c);
       }
-    float4 x0 = reinterpret_cast<float4*>(x + c)[0];
-    float4 x1 = reinterpret_cast<float4*>(x + c)[1];
+    float4 x0 = xn0, x1 = xn1;
+    if (c + kCombThreads * 8 < H) {
+      xn0 = reinterpret_cast<float4*>(x + c + kCombThreads * 8)[0];
+      xn1 = reinterpret_cast<float4*>(x + c + kCombThreads * 8)[1];
+    }
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int r = 0; r < NS; ++r) {
