@@ -420,6 +420,44 @@ def test_route_nan_logits_pick_distinct_experts(name, device):
     assert np.isnan(w[5]).all()
 
 
+@pytest.mark.parametrize("name", ["mixtral_bf16", "qwen_moe_bf16", "dsv3_share_bf16", "tiny_f32"])
+def test_route_exact_ties_and_special_values(name, device):
+    """Zero router rows make every logit its bias, so crafted biases put exact
+    ties (equal values, +0 against -0), infinities, NaN and subnormal values
+    among the logits: every token's picks are the oracle's stable top-k of
+    the GPU's own logits (larger first, ties to the lower id, NaN last) and
+    the counts follow them.  Covers the one-workgroup-per-token router
+    (E = 8), the matrix-core routers with 8 lanes per token (E = 60, 256) and
+    the fp32 path."""
+    B = _binding()
+    cfg = BY_NAME[name] if name == "tiny_f32" else mini(BY_NAME[name])
+    log(f"route ties {cfg.name}")
+    inp = DeviceInputs(cfg, device, weights=False)
+    desc = B.make_desc(cfg.L, cfg.H, cfg.F, cfg.E, cfg.k, cfg.S, cfg.D, cfg.dtype, cfg.eps)
+    tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    T = min(cfg.T, 96)
+    specials = np.array([1.0, 1.0, 0.0, -0.0, 2.0 ** -130, -1.0, np.inf, -np.inf, np.nan, 1.0, -0.0, 0.5],
+                        np.float32)
+    rng = np.random.default_rng(cfg.seed)
+    for trial in range(3):
+        pick = rng.integers(0, len(specials), size=cfg.E) if trial else np.arange(cfg.E) % len(specials)
+        bias = torch.from_numpy(specials[pick]).to(device)
+        Wg = torch.zeros_like(inp.Wg[0])
+        x = inp.x0[0, :T].clone()
+        a = torch.empty(T, cfg.H, dtype=tdt, device=device)
+        z = torch.empty(T, cfg.E, dtype=torch.float32, device=device)
+        idx = torch.empty(T, cfg.k, dtype=torch.int32, device=device)
+        w = torch.empty(T, cfg.k, dtype=torch.float32, device=device)
+        counts = torch.empty(cfg.E, dtype=torch.int32, device=device)
+        B.easybalance_route(desc, 0, T, x, inp.g[0], Wg, bias, a, z, idx, w, counts)
+        torch.cuda.synchronize()
+        zg = z.cpu().numpy()
+        got = idx.cpu().numpy()
+        assert np.array_equal(got, omodel.topk_indices(zg.astype(np.float64), cfg.k)), trial
+        assert all(len(set(r)) == cfg.k for r in got.tolist())
+        assert np.array_equal(counts.cpu().numpy(), omodel.expert_counts(got, cfg.E))
+
+
 def test_route_stage_one_workgroup_per_token_bf16(device):
     """bf16 stacks with E <= 8 and H > 4096 route one token per workgroup
     (the LDS-staged wavefront router holds H <= 4096): the same parity as
