@@ -57,6 +57,62 @@ def measured_traffic(config: str):
     return t.get("hbm_bytes_per_launch")
 
 
+def gateup_roofline(cfg, pairs: int, groups: int, t_s: float, launches: int, traffic) -> dict:
+    """Roofline entry of the grouped gate/up GEMM over launches that together
+    hold `pairs` (token, expert) pairs in `groups` distinct (layer, expert)
+    groups and took t_s seconds: algorithmic FLOP (4 H F per pair: gate and
+    up) and bytes (each group's gate/up weights once, each pair's A row read
+    and h row written), the bound whichever takes longer at the peak, and
+    both fractions."""
+    eb = 2 if cfg.dtype == "bf16" else 4
+    flop = 4 * cfg.H * cfg.F * pairs
+    nbytes = groups * 2 * cfg.F * cfg.H * eb + pairs * (cfg.H + cfg.F) * eb
+    peak_flops = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_FP32_VALU_TFLOPS
+    compute_s = flop / (peak_flops * 1e12)
+    memory_s = nbytes / (PEAK_HBM_GBS * 1e9)
+    if compute_s >= memory_s:
+        ach = flop / t_s / 1e12
+        roof = {"bound": "mfma" if cfg.dtype == "bf16" else "alu", "achieved": ach,
+                "peak": peak_flops, "unit": "TFLOP/s", "frac": ach / peak_flops, "traffic": traffic}
+    else:
+        ach = nbytes / t_s / 1e9
+        roof = {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": ach / PEAK_HBM_GBS, "traffic": traffic}
+    # both fractions, whichever bound applies: the MFMA share is the figure the
+    # 60%-of-bf16-peak target is stated in
+    roof["mfma_frac"] = flop / t_s / 1e12 / peak_flops
+    roof["hbm_frac"] = nbytes / t_s / 1e9 / PEAK_HBM_GBS
+    n = max(launches, 1)
+    roof.update({"kernel": "grouped_gemm_bf16<gate/up+SwiGLU>" if cfg.dtype == "bf16" else "grouped_gemm_f32<gate/up>",
+                 "launches": launches, "avg_launch_ms": t_s * 1e3 / n,
+                 "algorithmic_flop_per_launch": flop / n,
+                 "algorithmic_bytes_per_launch": nbytes / n,
+                 "time_at_mfma_peak_ms": compute_s * 1e3 / n,
+                 "time_at_hbm_peak_ms": memory_s * 1e3 / n})
+    return roof
+
+
+def kernel_algorithmic_bytes(cfg, tokens: int, pairs: int, groups: int, route_launches: int) -> dict:
+    """Algorithmic HBM bytes of the memory-bound kernel classes (and the down
+    GEMM) for a span of work that routes `tokens` (micro-batch, layer) tokens,
+    groups `pairs` (token, expert) pairs in `groups` distinct (layer, expert)
+    groups, with `route_launches` routing launches."""
+    eb = 2 if cfg.dtype == "bf16" else 4
+    return {
+        # x read (fp32), a written, logits / picks / weights written, each
+        # launch's router rows read once
+        "route_logits": tokens * (4 * cfg.H + eb * cfg.H + 4 * cfg.E + 8 * cfg.k)
+                        + route_launches * cfg.E * cfg.H * eb,
+        # grouped rows: a token's row read once, written per pair
+        "perm_gather": (tokens + pairs) * cfg.H * eb,
+        # o rows read per pair (and its routing weight and position), x read
+        # and written per token
+        "combine": pairs * (cfg.H * eb + 8) + tokens * 8 * cfg.H,
+        # weights of the distinct groups, h read, o written
+        "down": groups * cfg.F * cfg.H * eb + pairs * (cfg.F + cfg.H) * eb,
+    }
+
+
 def cpu_baseline(cfg, budget_s: float) -> dict:
     """The oracle (float64 NumPy) on whole MoE layers of the same stack, layer
     by layer over all micro-batches (each carrying its hidden state forward),
@@ -205,52 +261,16 @@ def main() -> int:
 
     # roofline of the grouped gate/up GEMM over the timed region
     gu_ms, gu_n = prof["gateup"]
-    eb = 2 if cfg.dtype == "bf16" else 4
-    gu_flop = 4 * cfg.H * cfg.F * pairs_pass * args.steps
     groups = sum(s.groups for s in steps) * args.steps
-    gu_bytes = (groups * 2 * cfg.F * cfg.H * eb
-                + pairs_pass * args.steps * (cfg.H + cfg.F) * eb)     # weights + A in + h out
-    t_gu = gu_ms / 1e3
+    roof = gateup_roofline(cfg, pairs_pass * args.steps, groups, gu_ms / 1e3, gu_n, measured_traffic(cfg.name))
     peak_flops = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_FP32_VALU_TFLOPS
-    compute_s = gu_flop / (peak_flops * 1e12)
-    memory_s = gu_bytes / (PEAK_HBM_GBS * 1e9)
-    traffic = measured_traffic(cfg.name)
-    if compute_s >= memory_s:
-        ach = gu_flop / t_gu / 1e12
-        roof = {"bound": "mfma" if cfg.dtype == "bf16" else "alu", "achieved": ach,
-                "peak": peak_flops, "unit": "TFLOP/s", "frac": ach / peak_flops, "traffic": traffic}
-    else:
-        ach = gu_bytes / t_gu / 1e9
-        roof = {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": ach / PEAK_HBM_GBS, "traffic": traffic}
-    # both fractions, whichever bound applies: the MFMA share is the figure the
-    # 60%-of-bf16-peak target is stated in
-    roof["mfma_frac"] = gu_flop / t_gu / 1e12 / peak_flops
-    roof["hbm_frac"] = gu_bytes / t_gu / 1e9 / PEAK_HBM_GBS
-    roof.update({"kernel": "grouped_gemm_bf16<gate/up+SwiGLU>" if cfg.dtype == "bf16" else "grouped_gemm_f32<gate/up>",
-                 "launches": gu_n, "avg_launch_ms": gu_ms / max(gu_n, 1),
-                 "algorithmic_flop_per_launch": gu_flop / max(gu_n, 1),
-                 "algorithmic_bytes_per_launch": gu_bytes / max(gu_n, 1),
-                 "time_at_mfma_peak_ms": compute_s * 1e3 / max(gu_n, 1),
-                 "time_at_hbm_peak_ms": memory_s * 1e3 / max(gu_n, 1)})
     kernels = {name: {"ms_per_pass": ms / n_bd, "launches_per_pass": n / n_bd}
                for name, (ms, n) in prof_all.items()}
     # algorithmic HBM bytes per pass of the memory-bound kernels (and the down
     # GEMM) against the 8 TB/s peak, from the per-kernel event times above
     tokens_pass = cfg.N * cfg.T * cfg.L            # every (micro-batch, layer) routed once
-    router_bytes = cfg.E * cfg.H * eb
-    alg_bytes = {
-        # x read (fp32), a written, logits / picks / weights written, each
-        # launch's router rows read once
-        "route_logits": tokens_pass * (4 * cfg.H + eb * cfg.H + 4 * cfg.E + 8 * cfg.k)
-                        + prof_all["route_logits"][1] / n_bd * router_bytes,
-        # grouped rows: a token's row read once, written per pair
-        "perm_gather": (tokens_pass + pairs_pass) * cfg.H * eb,
-        # o rows read per pair, x read and written per token, weights and rows
-        "combine": pairs_pass * (cfg.H * eb + 8) + tokens_pass * 8 * cfg.H,
-        # weights of the distinct groups, h read, o written
-        "down": groups / args.steps * cfg.F * cfg.H * eb + pairs_pass * (cfg.F + cfg.H) * eb,
-    }
+    alg_bytes = kernel_algorithmic_bytes(cfg, tokens_pass, pairs_pass, groups // args.steps,
+                                         round(prof_all["route_logits"][1] / n_bd))
     for name, b in alg_bytes.items():
         ms = kernels[name]["ms_per_pass"]
         kernels[name]["algorithmic_bytes_per_pass"] = b
