@@ -604,20 +604,32 @@ __global__ __launch_bounds__(256, KC == 2 ? 8 : 1) void route_token_kernel(RBA r
 // Router logits on the matrix cores and top-k (bf16 stacks, E <= 64).
 // A workgroup takes 32 tokens and all experts (padded to NB blocks of 32);
 // its 4 wavefronts split K into quarters, each accumulating a 32 x 32 NB
-// partial with v_mfma_f32_32x32x16_bf16 from operands loaded straight from L2
-// into registers (a ring of 32-wide K chunks in flight).  Waves 1..3 leave their
-// partials in LDS and wave 0 adds them in that order, then the bias (a fixed
-// summation order), and writes the logits to z and to an LDS tile from which
-// 8 lanes per token pick its top-k.
+// partial with v_mfma_f32_32x32x16_bf16.  Each wavefront streams its quarter
+// through a private LDS ring of kRouteKStages stages of 64 K columns, filled
+// by buffer loads straight into LDS (8 rows x 128 bytes, whole cache lines,
+// per load; 16-byte chunks XOR-swizzled as in the 128-token form below), so
+// the K loop needs no barrier.  Waves 1..3 leave their partials in LDS and
+// wave 0 adds them in that order, then the bias (a fixed summation order),
+// and writes the logits to z and to an LDS tile from which 8 lanes per token
+// pick its top-k; partials and tile reuse the rings.
+constexpr int kRouteKStages = 3;
+
 template <int NB, class RBA>
 __global__ __launch_bounds__(256) void route_mfma_kernel(RBA rba, int H, int E, int k,
                                                          int norm_topk) {
-  constexpr int ZS = NB * 32 + 1;  // padded LDS row of the logit tile
-  __shared__ float part[3][NB][16][64];
-  __shared__ float zs[32][ZS];
+  constexpr int ZS = NB * 32 + 1;                 // padded LDS row of the logit tile
+  constexpr int SLOT = (32 + NB * 32) * 64;       // one stage: 32 token rows, NB*32 router rows
+  constexpr int WRING = kRouteKStages * SLOT;     // one wavefront's ring
+  constexpr int kALd = 4, kBLd = 4 * NB;          // 1 KB loads of one stage
+  constexpr int kAhead = (kALd + kBLd) * (kRouteKStages - 1);
+  static_assert(kAhead < 64, "vmcnt range");
+  static_assert((3 * NB * 16 * 64 + 32 * ZS) * 4 <= 4 * WRING * 2, "partials and logit tile fit in the rings");
+  __shared__ __attribute__((aligned(1024))) bf16_t ring[4 * WRING];
+  // the rings are written by global->LDS loads the compiler does not see
+  asm volatile("" ::"v"(ring) : "memory");
   const RouteBatch& rb = rba.get();
   if ((int)blockIdx.x >= rb.blk0[rb.n]) return;  // past the live 32-token blocks
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lrow = lane & 31, khalf = lane >> 5;
   const int ei = find_entry(rb.blk0, rb.n, blockIdx.x);
   const int T = rb.tok0[ei + 1] - rb.tok0[ei];
@@ -628,51 +640,72 @@ __global__ __launch_bounds__(256) void route_mfma_kernel(RBA rba, int H, int E, 
   float* __restrict__ z = in_global(rb.e[ei].z);
   int32_t* __restrict__ idx = in_global(rb.e[ei].idx);
   float* __restrict__ w = in_global(rb.e[ei].w);
-  const int kq = H / 4, kbeg = wave * kq;
-  // this lane's A row (token) and B rows (experts), clamped into range
-  const bf16_t* arow = a + (size_t)min(t0 + lrow, T - 1) * H + kbeg + 8 * khalf;
-  const bf16_t* brow[NB];
+  // buffer descriptors: token rows past T and router rows past E read zeros
+  // (their logits are never used)
+  const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<bf16_t*>(a + (size_t)t0 * H), (short)0, min(T - t0, 32) * H * 2, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<bf16_t*>(Wg), (short)0, (int)(E * H * 2), 0x00020000);
+  // load lane l: row l / 8 of an 8-row block, physical chunk l % 8 holding
+  // logical chunk (l % 8) ^ ((row >> 1) & 7) (row counted within the token or
+  // router rows; odd blocks flip bit 2)
+  const int lr = lane >> 3, lp = lane & 7;
+  const int c_even = lp ^ ((lr >> 1) & 7), c_odd = c_even ^ 4;
+  const int row_b = 2 * H;  // bytes of one row
+  const int voff_even = lr * row_b + c_even * 16, voff_odd = lr * row_b + c_odd * 16;
+  const int kq = H / 4, kbeg = wave * kq, nst = kq / 64;
+  bf16_t* wring = ring + wave * WRING;
+  auto issue = [&](int st, int slot) {
+    st = min(st, nst - 1);  // past the last stage: reload it into a slot nobody reads
+    bf16_t* sa = wring + slot * SLOT;
+    const int koff = (kbeg + 64 * st) * 2;
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb)
-    brow[nb] = Wg + (size_t)min(nb * 32 + lrow, E - 1) * H + kbeg + 8 * khalf;
+    for (int j = 0; j < kALd; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, sa + 8 * j * 64, 16, (j & 1) ? voff_odd : voff_even,
+                                               8 * j * row_b + koff, 0, 0);
+#pragma unroll
+    for (int j = 0; j < kBLd; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, sa + (32 + 8 * j) * 64, 16, (j & 1) ? voff_odd : voff_even,
+                                               8 * j * row_b + koff, 0, 0);
+  };
   floatx16_t acc[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
     for (int v = 0; v < 16; ++v) acc[nb][v] = 0.f;
-  // a 32-wide K chunk = two MFMA k-steps of 16; a ring of D chunks in flight
-  constexpr int D = NB <= 4 ? 4 : 2;
-  bf16x8_t ac[D][2], bc[D][NB][2];
-  auto load = [&](int buf, int kk) {
+  const int sw = (lrow >> 1) & 7;
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      ac[buf][s] = *reinterpret_cast<const bf16x8_t*>(arow + kk + 16 * s);
+  for (int st = 0; st < kRouteKStages - 1; ++st) issue(st, st);
+  for (int st = 0; st < nst; ++st) {
+    // this wavefront's fragment reads of stage st-1 are done before its slot
+    // is refilled with stage st+2; stage st has landed once only the two later
+    // stages' loads are in flight (loads complete in issue order)
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4));  // lgkmcnt(0)
+    issue(st + kRouteKStages - 1, (st + kRouteKStages - 1) % kRouteKStages);
+    __builtin_amdgcn_s_waitcnt((kAhead & 15) | ((kAhead >> 4) << 14) | (7 << 4));
+    asm volatile("" ::: "memory");
+    const bf16_t* sa = wring + (st % kRouteKStages) * SLOT;
+    const bf16_t* sb = sa + 32 * 64;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const int ch = ((2 * ks + khalf) ^ sw) * 8;
+      const bf16x8_t af = *reinterpret_cast<const bf16x8_t*>(sa + lrow * 64 + ch);
+      bf16x8_t bfr[NB];
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) bfr[nb] = *reinterpret_cast<const bf16x8_t*>(sb + (nb * 32 + lrow) * 64 + ch);
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
-        bc[buf][nb][s] = *reinterpret_cast<const bf16x8_t*>(brow[nb] + kk + 16 * s);
-    }
-  };
-  auto mma = [&](int buf) {
-#pragma unroll
-    for (int s = 0; s < 2; ++s)
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-        acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ac[buf][s], bc[buf][nb][s], acc[nb], 0, 0, 0);
-  };
-  const int nch = kq / 32;
-#pragma unroll
-  for (int d = 0; d < D; ++d)
-    if (d < nch) load(d, 32 * d);
-  for (int c0 = 0; c0 < nch; c0 += D) {
-#pragma unroll
-    for (int d = 0; d < D; ++d) {
-      const int c = c0 + d;
-      if (c < nch) {
-        mma(d);
-        if (c + D < nch) load(d, 32 * (c + D));
-      }
+        acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, bfr[nb], acc[nb], 0, 0, 0);
     }
   }
+  // every load (the reloads past the last stage included) has landed and
+  // every wave is done with its ring before the partials overwrite them
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(7 << 4);
+  __syncthreads();
+  float(*part)[NB][16][64] = reinterpret_cast<float(*)[NB][16][64]>(ring);
+  float(*zs)[ZS] = reinterpret_cast<float(*)[ZS]>(reinterpret_cast<float*>(ring) + 3 * NB * 16 * 64);
   if (wave > 0) {
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb)
