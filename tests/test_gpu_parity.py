@@ -66,8 +66,11 @@ LIMIT_CFGS = [
 LIMIT_IDS = [c.name for c in LIMIT_CFGS]
 # the RMSNorm in front of the separate router kernels, by row length: a
 # workgroup per token holding 4 float4 of the row per thread (2048 < H <=
-# 4096), 8 (4096 < H <= 8192), and one wavefront per token above that
+# 4096), 8 (4096 < H <= 8192), and one wavefront per token above that; and
+# the matrix-core router with most of its 64 expert rows padding (E = 20)
 NORM_CFGS = [
+    Config("experts20_bf16", L=1, H=512, F=128, E=20, k=3, S=0, D=4, N=2, T=70, dtype="bf16",
+           skew="zipf", skew_param=1.1, seed=20261013),
     Config("norm4_bf16", L=1, H=4096, F=128, E=64, k=4, S=0, D=4, N=2, T=70, dtype="bf16",
            skew="zipf", skew_param=1.1, seed=20261010),
     Config("norm8_f32", L=1, H=5120, F=128, E=96, k=3, S=0, D=4, N=2, T=70, dtype="f32",
