@@ -77,6 +77,8 @@ NORM_CFGS = [
            skew="dirichlet", skew_param=0.3, seed=20261011),
     Config("normwave_bf16", L=1, H=8448, F=128, E=100, k=6, S=0, D=4, N=2, T=70, dtype="bf16",
            skew="dirichlet", skew_param=0.3, seed=20261012),
+    Config("normwave64_bf16", L=1, H=8448, F=128, E=64, k=6, S=0, D=4, N=2, T=70, dtype="bf16",
+           skew="dirichlet", skew_param=0.3, seed=20261014),
 ]
 NORM_IDS = [c.name for c in NORM_CFGS]
 
